@@ -1,0 +1,179 @@
+/*
+ * elas.h -- C ABI of the MI355X (gfx950) implementation of the ELAS low-rank
+ * FFN with 2:4 activation sparsity (ELAS, arXiv 2605.03667).
+ *
+ * The block (Fig. 1 caption; Eq. 1-3, Algorithm 1), tokens as rows:
+ *
+ *     P = x U_up                x [T,d], U_up [d,r]          (Eq. 1 factors)
+ *     H = P V_up                V_up [r,d_ff]
+ *     s = max(0,H)^2            Eq. 2
+ *     S = mask_top2(s) * s      Algorithm 1 / Eq. 3, groups of 4 along d_ff
+ *     Z = S U_down              U_down [d_ff,r]  (2:4 sparse x dense GEMM)
+ *     Y = Z V_down              V_down [r,d]
+ *
+ * With W = A B of Eq. 1 acting on row vectors, U = B^T and V = A^T.
+ *
+ * Conventions shared by every entry point
+ * ----------------------------------------
+ * - bf16 tensors are passed as uint16_t bit patterns; float32 as float.
+ * - Every tensor pointer is a DEVICE pointer owned by the caller.  The library
+ *   never allocates, frees or keeps device memory (workspace is the caller's).
+ * - Dense tensors are row-major and contiguous.  Every pointer must be 16-byte
+ *   aligned.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *   work is enqueued on it asynchronously; the calls do not synchronise.
+ * - Arguments are validated on the host before anything is enqueued.  On an
+ *   error nothing is launched, outputs are untouched, the return value is the
+ *   error code and elas_last_error() (thread-local) describes it.  A failed
+ *   kernel launch returns ELAS_ERR_DEVICE; faults inside kernels surface at the
+ *   caller's next synchronisation, as for any HIP work.
+ * - Calls on one stream are ordered; calls that share output or workspace
+ *   buffers must not run concurrently on different streams.
+ *
+ * Compressed 2:4 layout ("sparse rows")
+ * -------------------------------------
+ * A matrix Z [M x N] whose every group of 4 consecutive row entries (features
+ * 4j..4j+3) keeps exactly 2 entries (Algorithm 1) is stored as
+ *   vals [M x ldv] bf16 : group j's kept values at vals[i][2j], vals[i][2j+1],
+ *                         in ascending feature order;
+ *   meta [M x ldm] bytes: group j's code  i0 | (i1 << 2)  (i0 < i1 are the
+ *                         kept positions inside the group) in byte j/2, low
+ *                         nibble for even j, high nibble for odd j.
+ * Row pitches: ldv = 32 * ceil(N/64) values and ldm = 8 * ceil(N/64) bytes
+ * (rows padded to a multiple of 64 features so every row is 16-byte aligned).
+ * Padding groups (j >= N/4) hold values 0 and code 0x4 (positions 0 and 1), so
+ * a padded row is itself a valid 2:4 row whose extra entries are zero.
+ * Per kept value this is 2 bytes plus 2 bits: 0.5625 of dense bf16, the ratio
+ * of the paper's Table 2 (Sec. 4.2.2).
+ */
+#ifndef ELAS_H
+#define ELAS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes -------------------------------------------------------- */
+#define ELAS_OK              0
+#define ELAS_ERR_NULL        1  /* a required pointer is NULL                      */
+#define ELAS_ERR_SHAPE       2  /* a size is out of range or not a required multiple */
+#define ELAS_ERR_ALIGN       3  /* a pointer is not 16-byte aligned                */
+#define ELAS_ERR_WORKSPACE   4  /* workspace missing or smaller than required      */
+#define ELAS_ERR_FLAGS       5  /* unknown or unsupported flag bits                */
+#define ELAS_ERR_DEVICE      6  /* a HIP call or kernel launch failed              */
+
+/* ---- flags ---------------------------------------------------------------- */
+/* elas_sparsify_24: what the top-2 selection ranks (Algorithm 1). */
+#define ELAS_SPARSIFY_RELU2  0u /* s = max(0,h)^2 is ranked and stored (ELAS's activation) */
+#define ELAS_SPARSIFY_RAW    1u /* h itself is ranked by |h| and stored unchanged          */
+
+/* elas_spmm_24: layout of the dense operand B. */
+#define ELAS_B_KN            0  /* B is [K x N] row-major                         */
+#define ELAS_B_NK            1  /* B is [N x K] row-major (B^T stored)            */
+
+/* Human-readable name of a status code (static string). */
+const char* elas_status_string(int status);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char* elas_last_error(void);
+
+/* Row pitches of the compressed layout for a row of N features:
+ * values per row (ldv) and metadata bytes per row (ldm).  N must be > 0. */
+int64_t elas_vals_ld(int64_t N);
+int64_t elas_meta_ld(int64_t N);
+
+/*
+ * elas_sparsify_24 -- Algorithm 1 (Sec. 3.3.1) with Eq. 2 in front of it.
+ *
+ * h     [M x N] bf16, device, read only.
+ * vals  [M x elas_vals_ld(N)] bf16, device, written (compressed layout above).
+ * meta  [M x elas_meta_ld(N)] bytes, device, written.
+ * flags ELAS_SPARSIFY_RELU2: key and value are s = max(0,h)^2 computed in fp32
+ *       (h*h is exact in fp32 for 2^-63 <= |h| < 2^64), ranked exactly as the
+ *       real numbers s, ties to the lower index; kept values are s rounded to
+ *       bf16, nearest-even.  relu(NaN) = 0.
+ *       ELAS_SPARSIFY_RAW: key |h|, kept values are h's bits unchanged.
+ * Requires M >= 0, N > 0, N % 8 == 0.  M == 0 is a no-op (pointers are then
+ * not inspected and may be NULL).
+ */
+int elas_sparsify_24(const uint16_t* h, int64_t M, int64_t N, uint32_t flags,
+                     uint16_t* vals, uint8_t* meta, void* stream);
+
+/*
+ * elas_spmm_24 -- C = A B with A 2:4-sparse along K (the paper's sparse x
+ * dense product of the down projection, Fig. 1 caption and Sec. 4.2.2).
+ *
+ * a_vals, a_meta  A [M x K] in the compressed layout (pitches for N := K).
+ * b               B, bf16, [K x N] (b_layout ELAS_B_KN) or [N x K] (ELAS_B_NK).
+ * c               C [M x N] bf16, written; products accumulate in fp32 and are
+ *                 rounded to bf16 (nearest-even) once.
+ * workspace       device scratch of at least elas_spmm_24_workspace_bytes()
+ *                 bytes (may be NULL when that is 0).
+ * Requires M >= 0, K > 0, K % 8 == 0, N > 0, N % 8 == 0, K and N at most 65536.
+ * M == 0 is a no-op (pointers are then not inspected and may be NULL).
+ */
+size_t elas_spmm_24_workspace_bytes(int64_t M, int64_t K, int64_t N, int b_layout);
+int elas_spmm_24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, int64_t K,
+                 const uint16_t* b, int64_t N, int b_layout, uint16_t* c,
+                 void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * elas_lowrank_ffn_fwd -- forward of the block above.
+ *
+ * Inputs (bf16, device, read only): x [T,d], U_up [d,r], V_up [r,d_ff],
+ *   U_down [d_ff,r], V_down [r,d].
+ * Outputs (bf16, device, written):
+ *   y      [T,d]
+ *   P      [T,r]   saved for the backward (P = x U_up, rounded to bf16)
+ *   s_vals [T x elas_vals_ld(d_ff)]  compressed S (kept s rounded to bf16)
+ *   s_meta [T x elas_meta_ld(d_ff)]  its 2-bit indices
+ *   Z      [T,r]   saved for the backward
+ * Rounding points: P, H (before ReLU^2), the kept s, Z and y are rounded to
+ * bf16 (nearest-even); every product accumulates in fp32.  The 2:4 selection
+ * ranks max(0, bf16(H))^2 exactly, ties to the lower index.
+ * workspace >= elas_lowrank_ffn_fwd_workspace_bytes(T, d, d_ff, r).
+ * flags must be 0.
+ * Requires T >= 0, d, d_ff, r > 0, multiples of 8 and at most 65536.  T == 0 is
+ * a no-op (pointers are then not inspected and may be NULL).
+ */
+size_t elas_lowrank_ffn_fwd_workspace_bytes(int64_t T, int64_t d, int64_t d_ff, int64_t r);
+int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t* V_up,
+                         const uint16_t* U_down, const uint16_t* V_down,
+                         int64_t T, int64_t d, int64_t d_ff, int64_t r, uint32_t flags,
+                         uint16_t* y, uint16_t* P, uint16_t* s_vals, uint8_t* s_meta,
+                         uint16_t* Z, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * elas_lowrank_ffn_bwd -- backward of the block (Sec. 3.3.2, Sec. 3.4).
+ *
+ * dy [T,d] bf16 is dL/dY; x, U_up, V_up, U_down, V_down as in the forward;
+ * P, s_vals, s_meta, Z are the forward's saved outputs (read only).
+ * Outputs: dx [T,d] bf16 (written); dU_up [d,r], dV_up [r,d_ff],
+ *   dU_down [d_ff,r], dV_down [r,d] fp32 (overwritten, not accumulated).
+ * Gradient through the activation: dH = dS * mask * 2 relu(H) with the stored
+ * mask, the derivative of the sparsified forward (relu(H) is recovered
+ * exactly from the stored bf16 s).  The full-width activation is never read:
+ * dU_down = S^T dZ uses the compressed S.
+ * Rounding points: dZ, dH (kept entries), dP and dx are rounded to bf16.
+ * workspace >= elas_lowrank_ffn_bwd_workspace_bytes(T, d, d_ff, r).
+ * flags must be 0.  Same size rules as the forward; T == 0 writes zero
+ * weight gradients (only the four gradient pointers and the workspace are
+ * then inspected).
+ */
+size_t elas_lowrank_ffn_bwd_workspace_bytes(int64_t T, int64_t d, int64_t d_ff, int64_t r);
+int elas_lowrank_ffn_bwd(const uint16_t* dy, const uint16_t* x, const uint16_t* U_up,
+                         const uint16_t* V_up, const uint16_t* U_down, const uint16_t* V_down,
+                         int64_t T, int64_t d, int64_t d_ff, int64_t r, uint32_t flags,
+                         const uint16_t* P, const uint16_t* s_vals, const uint8_t* s_meta,
+                         const uint16_t* Z,
+                         uint16_t* dx, float* dU_up, float* dV_up, float* dU_down, float* dV_down,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ELAS_H */

@@ -1,0 +1,221 @@
+"""Python binding of libelas, the MI355X (gfx950) ELAS low-rank 2:4 FFN.
+
+Thin ctypes wrapper over the C ABI declared in ``include/elas.h``: the
+functions here carry the same names as the C entry points and only marshal
+arguments (torch tensors -> device pointers and sizes, the current HIP stream,
+output and workspace tensors).  Every step of the computation runs in the HIP
+kernels of ``libelas.so``; there is no fallback: if the library is not built,
+or a tensor is not on the GPU, the call raises.
+
+bf16 tensors use ``torch.bfloat16``; the compressed 2:4 metadata uses
+``torch.uint8``; weight gradients are ``torch.float32``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "ElasError", "lib", "elas_vals_ld", "elas_meta_ld", "elas_sparsify_24", "elas_spmm_24",
+    "elas_spmm_24_workspace_bytes", "elas_lowrank_ffn_fwd", "elas_lowrank_ffn_fwd_workspace_bytes",
+    "elas_lowrank_ffn_bwd", "elas_lowrank_ffn_bwd_workspace_bytes",
+    "ELAS_SPARSIFY_RELU2", "ELAS_SPARSIFY_RAW", "ELAS_B_KN", "ELAS_B_NK",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libelas.so")
+
+ELAS_SPARSIFY_RELU2 = 0
+ELAS_SPARSIFY_RAW = 1
+ELAS_B_KN = 0
+ELAS_B_NK = 1
+
+_STATUS = {0: "ELAS_OK", 1: "ELAS_ERR_NULL", 2: "ELAS_ERR_SHAPE", 3: "ELAS_ERR_ALIGN",
+           4: "ELAS_ERR_WORKSPACE", 5: "ELAS_ERR_FLAGS", 6: "ELAS_ERR_DEVICE"}
+
+
+class ElasError(RuntimeError):
+    def __init__(self, code: int, detail: str):
+        super().__init__(f"{_STATUS.get(code, code)}: {detail}")
+        self.code = code
+        self.detail = detail
+
+
+_lib = None
+_p = ctypes.c_void_p
+_i64 = ctypes.c_int64
+_u32 = ctypes.c_uint32
+_sz = ctypes.c_size_t
+
+_SIGNATURES = {
+    "elas_status_string": ([ctypes.c_int], ctypes.c_char_p),
+    "elas_last_error": ([], ctypes.c_char_p),
+    "elas_vals_ld": ([_i64], _i64),
+    "elas_meta_ld": ([_i64], _i64),
+    "elas_sparsify_24": ([_p, _i64, _i64, _u32, _p, _p, _p], ctypes.c_int),
+    "elas_spmm_24_workspace_bytes": ([_i64, _i64, _i64, ctypes.c_int], _sz),
+    "elas_spmm_24": ([_p, _p, _i64, _i64, _p, _i64, ctypes.c_int, _p, _p, _sz, _p], ctypes.c_int),
+    "elas_lowrank_ffn_fwd_workspace_bytes": ([_i64, _i64, _i64, _i64], _sz),
+    "elas_lowrank_ffn_fwd": ([_p] * 5 + [_i64] * 4 + [_u32] + [_p] * 5 + [_p, _sz, _p], ctypes.c_int),
+    "elas_lowrank_ffn_bwd_workspace_bytes": ([_i64, _i64, _i64, _i64], _sz),
+    "elas_lowrank_ffn_bwd": ([_p] * 6 + [_i64] * 4 + [_u32] + [_p] * 4 + [_p] * 5 + [_p, _sz, _p],
+                             ctypes.c_int),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libelas.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2605_03667_amd.build`")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGNATURES.items():
+            f = getattr(handle, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = handle
+    return _lib
+
+
+def _check(rc: int) -> None:
+    if rc != 0:
+        raise ElasError(rc, lib().elas_last_error().decode())
+
+
+def _ptr(t: torch.Tensor | None, dtype: torch.dtype, name: str):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _workspace(nbytes: int, device: torch.device) -> torch.Tensor | None:
+    if nbytes == 0:
+        return None
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def elas_vals_ld(N: int) -> int:
+    return lib().elas_vals_ld(N)
+
+
+def elas_meta_ld(N: int) -> int:
+    return lib().elas_meta_ld(N)
+
+
+def elas_sparsify_24(h: torch.Tensor, flags: int = ELAS_SPARSIFY_RELU2, vals: torch.Tensor | None = None,
+                     meta: torch.Tensor | None = None):
+    """2:4 sparsification of h [M, N] (bf16).  Returns (vals, meta)."""
+    M, N = h.shape
+    if vals is None:
+        vals = torch.empty((M, elas_vals_ld(N)), dtype=torch.bfloat16, device=h.device)
+    if meta is None:
+        meta = torch.empty((M, elas_meta_ld(N)), dtype=torch.uint8, device=h.device)
+    _check(lib().elas_sparsify_24(_ptr(h, torch.bfloat16, "h"), M, N, flags,
+                                  _ptr(vals, torch.bfloat16, "vals"), _ptr(meta, torch.uint8, "meta"),
+                                  _stream(h.device)))
+    return vals, meta
+
+
+def elas_spmm_24_workspace_bytes(M: int, K: int, N: int, b_layout: int) -> int:
+    return lib().elas_spmm_24_workspace_bytes(M, K, N, b_layout)
+
+
+def elas_spmm_24(a_vals: torch.Tensor, a_meta: torch.Tensor, K: int, b: torch.Tensor,
+                 b_layout: int = ELAS_B_KN, c: torch.Tensor | None = None,
+                 workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """C [M, N] = A B with A 2:4-compressed [M, K] (vals, meta) and B [K, N]
+    (ELAS_B_KN) or [N, K] (ELAS_B_NK)."""
+    M = a_vals.shape[0]
+    N = b.shape[1] if b_layout == ELAS_B_KN else b.shape[0]
+    if c is None:
+        c = torch.empty((M, N), dtype=torch.bfloat16, device=a_vals.device)
+    need = elas_spmm_24_workspace_bytes(M, K, N, b_layout)
+    if workspace is None:
+        workspace = _workspace(need, a_vals.device)
+    _check(lib().elas_spmm_24(_ptr(a_vals, torch.bfloat16, "a_vals"), _ptr(a_meta, torch.uint8, "a_meta"), M, K,
+                              _ptr(b, torch.bfloat16, "b"), N, b_layout, _ptr(c, torch.bfloat16, "c"),
+                              _ptr(workspace, torch.uint8, "workspace"),
+                              0 if workspace is None else workspace.numel(), _stream(a_vals.device)))
+    return c
+
+
+def elas_lowrank_ffn_fwd_workspace_bytes(T: int, d: int, d_ff: int, r: int) -> int:
+    return lib().elas_lowrank_ffn_fwd_workspace_bytes(T, d, d_ff, r)
+
+
+def elas_lowrank_ffn_bwd_workspace_bytes(T: int, d: int, d_ff: int, r: int) -> int:
+    return lib().elas_lowrank_ffn_bwd_workspace_bytes(T, d, d_ff, r)
+
+
+def elas_lowrank_ffn_fwd(x, U_up, V_up, U_down, V_down, flags: int = 0, out: dict | None = None,
+                         workspace: torch.Tensor | None = None) -> dict:
+    """Forward of the low-rank 2:4 FFN.  Returns dict(y, P, s_vals, s_meta, Z)."""
+    T, d = x.shape
+    r = U_up.shape[1]
+    F = V_up.shape[1]
+    dev = x.device
+    if out is None:
+        out = {
+            "y": torch.empty((T, d), dtype=torch.bfloat16, device=dev),
+            "P": torch.empty((T, r), dtype=torch.bfloat16, device=dev),
+            "s_vals": torch.empty((T, elas_vals_ld(F)), dtype=torch.bfloat16, device=dev),
+            "s_meta": torch.empty((T, elas_meta_ld(F)), dtype=torch.uint8, device=dev),
+            "Z": torch.empty((T, r), dtype=torch.bfloat16, device=dev),
+        }
+    need = elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r)
+    if workspace is None:
+        workspace = _workspace(need, dev)
+    bf = torch.bfloat16
+    _check(lib().elas_lowrank_ffn_fwd(
+        _ptr(x, bf, "x"), _ptr(U_up, bf, "U_up"), _ptr(V_up, bf, "V_up"), _ptr(U_down, bf, "U_down"),
+        _ptr(V_down, bf, "V_down"), T, d, F, r, flags,
+        _ptr(out["y"], bf, "y"), _ptr(out["P"], bf, "P"), _ptr(out["s_vals"], bf, "s_vals"),
+        _ptr(out["s_meta"], torch.uint8, "s_meta"), _ptr(out["Z"], bf, "Z"),
+        _ptr(workspace, torch.uint8, "workspace"), 0 if workspace is None else workspace.numel(),
+        _stream(dev)))
+    return out
+
+
+def elas_lowrank_ffn_bwd(dy, x, U_up, V_up, U_down, V_down, saved: dict, flags: int = 0,
+                         grads: dict | None = None, workspace: torch.Tensor | None = None) -> dict:
+    """Backward of the low-rank 2:4 FFN given the forward's saved tensors
+    (P, s_vals, s_meta, Z).  Returns dict(dx, dU_up, dV_up, dU_down, dV_down)."""
+    T, d = x.shape
+    r = U_up.shape[1]
+    F = V_up.shape[1]
+    dev = x.device
+    if grads is None:
+        f32 = torch.float32
+        grads = {
+            "dx": torch.empty((T, d), dtype=torch.bfloat16, device=dev),
+            "dU_up": torch.empty((d, r), dtype=f32, device=dev),
+            "dV_up": torch.empty((r, F), dtype=f32, device=dev),
+            "dU_down": torch.empty((F, r), dtype=f32, device=dev),
+            "dV_down": torch.empty((r, d), dtype=f32, device=dev),
+        }
+    need = elas_lowrank_ffn_bwd_workspace_bytes(T, d, F, r)
+    if workspace is None:
+        workspace = _workspace(need, dev)
+    bf, f32 = torch.bfloat16, torch.float32
+    _check(lib().elas_lowrank_ffn_bwd(
+        _ptr(dy, bf, "dy"), _ptr(x, bf, "x"), _ptr(U_up, bf, "U_up"), _ptr(V_up, bf, "V_up"),
+        _ptr(U_down, bf, "U_down"), _ptr(V_down, bf, "V_down"), T, d, F, r, flags,
+        _ptr(saved["P"], bf, "P"), _ptr(saved["s_vals"], bf, "s_vals"),
+        _ptr(saved["s_meta"], torch.uint8, "s_meta"), _ptr(saved["Z"], bf, "Z"),
+        _ptr(grads["dx"], bf, "dx"), _ptr(grads["dU_up"], f32, "dU_up"), _ptr(grads["dV_up"], f32, "dV_up"),
+        _ptr(grads["dU_down"], f32, "dU_down"), _ptr(grads["dV_down"], f32, "dV_down"),
+        _ptr(workspace, torch.uint8, "workspace"), 0 if workspace is None else workspace.numel(),
+        _stream(dev)))
+    return grads

@@ -1,0 +1,317 @@
+// Launch sequences of the ELAS low-rank 2:4 FFN on one GPU: forward (ELAS
+// Fig. 1 caption; Eq. 1-3, Algorithm 1), backward (Sec. 3.3.2, Sec. 3.4) and
+// the standalone 2:4 sparse x dense product.  Everything runs on the caller's
+// stream in the caller's workspace; nothing here allocates.
+#include "gemm.h"
+#include "internal.h"
+
+namespace elas {
+
+namespace {
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Carves consecutive aligned regions out of the caller's workspace.
+struct Carver {
+  char* p;
+  size_t used = 0;
+  template <class T>
+  T* take(size_t count) {
+    T* r = p ? (T*)(p + used) : nullptr;
+    used += align_up(count * sizeof(T));
+    return r;
+  }
+};
+
+// ---- small kernels -----------------------------------------------------------
+
+// out[j][i] = in[i][j] for i < rows, j < cols; 0 elsewhere in [out_rows x out_cols].
+__global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __restrict__ in, int64_t rows,
+                                                            int64_t cols, int64_t ldi, uint16_t* __restrict__ out,
+                                                            int64_t out_rows, int64_t out_cols, int64_t ldo) {
+  __shared__ uint16_t tile[64][65];
+  const int64_t i0 = (int64_t)blockIdx.x * 64, j0 = (int64_t)blockIdx.y * 64;
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int a = e / 64, b = e % 64;
+    const int64_t i = i0 + a, j = j0 + b;
+    tile[a][b] = (i < rows && j < cols) ? in[i * ldi + j] : (uint16_t)0;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int a = e / 64, b = e % 64;
+    const int64_t jj = j0 + a, ii = i0 + b;
+    if (jj < out_rows && ii < out_cols) out[jj * ldo + ii] = tile[b][a];
+  }
+}
+
+hipError_t transpose_pad(const uint16_t* in, int64_t rows, int64_t cols, int64_t ldi, uint16_t* out,
+                         int64_t out_rows, int64_t out_cols, int64_t ldo, hipStream_t st) {
+  const dim3 grid((unsigned)cdiv(out_cols, 64), (unsigned)cdiv(out_rows, 64));
+  hipLaunchKernelGGL(transpose_pad_kernel, grid, dim3(256), 0, st, in, rows, cols, ldi, out, out_rows, out_cols,
+                     ldo);
+  return hipGetLastError();
+}
+
+// out = sum over splits of part[s] (fixed order, so the result is
+// deterministic); rows m < rows_out only; optionally transposed.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int splits, int64_t M,
+                                                            int64_t N, int64_t rows_out, int transpose,
+                                                            float* __restrict__ out, int64_t ldo) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= rows_out * N) return;
+  int64_t m, n;
+  if (transpose) {   // consecutive threads walk m so the transposed writes are contiguous
+    n = e / rows_out;
+    m = e - n * rows_out;
+  } else {
+    m = e / N;
+    n = e - m * N;
+  }
+  float s = 0.f;
+  for (int k = 0; k < splits; ++k) s += part[(int64_t)k * M * N + m * N + n];
+  if (transpose)
+    out[n * ldo + m] = s;
+  else
+    out[m * ldo + n] = s;
+}
+
+__global__ __launch_bounds__(256) void fill_zero_kernel(float* __restrict__ p, int64_t n) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e < n) p[e] = 0.f;
+}
+
+hipError_t fill_zero(float* p, int64_t n, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, p, n);
+  return hipGetLastError();
+}
+
+// ---- GEMM configurations -----------------------------------------------------
+// Dense C = A B^T-style products with both operands K-contiguous.
+template <int BN, int EPI, bool M_FAST>
+using CfgNT = GemmCfg<256, BN, 2, 2, OP_K, OP_K, EPI, M_FAST>;
+// 2:4 sparse A (smfmac) times K-contiguous B.
+using CfgSP = GemmCfg<256, 128, 2, 2, OP_SP, OP_K, EPI_BF16, false>;
+// Contraction over tokens (K = T): both operands stored [T x rows].
+template <int AMODE>
+using CfgTT = GemmCfg<256, 256, 2, 2, AMODE, OP_T, EPI_F32, false>;
+
+template <class Cfg>
+hipError_t launch(GemmArgs g, int splits, hipStream_t st) {
+  g.tiles_m = (int)cdiv(g.M, Cfg::BM);
+  g.tiles_n = (int)cdiv(g.N, Cfg::BN);
+  if (splits <= 1) {
+    splits = 1;
+    g.k_split = cdiv(g.K, Cfg::BK) * Cfg::BK;
+  }
+  const dim3 grid((unsigned)(g.tiles_m * g.tiles_n), (unsigned)splits);
+  hipLaunchKernelGGL(gemm_kernel<Cfg>, grid, dim3(256), 0, st, g);
+  return hipGetLastError();
+}
+
+// Dense product C[M x N] = A[M x K] * Bt[N x K]^T in bf16.
+hipError_t gemm_nt_bf16(const uint16_t* A, int64_t lda, const uint16_t* Bt, int64_t ldb, uint16_t* C, int64_t ldc,
+                        int64_t M, int64_t N, int64_t K, hipStream_t st) {
+  GemmArgs g{};
+  g.A = A; g.lda = lda; g.B = Bt; g.ldb = ldb; g.C = C; g.ldc = ldc;
+  g.M = M; g.N = N; g.K = K; g.m_valid = M; g.ka_valid = K; g.kb_valid = K;
+  if (N <= 128) return launch<CfgNT<128, EPI_BF16, false>>(g, 1, st);
+  return launch<CfgNT<256, EPI_BF16, false>>(g, 1, st);
+}
+
+// Split plan of a K = T product: enough workgroups to cover the 256 CUs once,
+// each split at least 8 K steps long.
+struct SplitPlan {
+  int splits;
+  int64_t k_split;
+};
+SplitPlan plan_splits(int64_t M, int64_t N, int64_t K) {
+  const int64_t tiles = cdiv(M, 256) * cdiv(N, 256);
+  const int64_t steps = cdiv(K, 64);
+  int64_t s = 256 / tiles;
+  if (s < 1) s = 1;
+  if (s > steps / 8) s = steps / 8 > 0 ? steps / 8 : 1;
+  const int64_t k_split = cdiv(cdiv(K, s), 64) * 64;
+  return {(int)cdiv(K, k_split), k_split};
+}
+size_t partial_bytes(int64_t M, int64_t N, int64_t K) {
+  const SplitPlan p = plan_splits(M, N, K);
+  return (size_t)p.splits * M * N * sizeof(float);
+}
+
+// C = A^T B summed over K = T rows, reduced into out (optionally transposed),
+// keeping rows m < rows_out.  A is [K x M] dense (OP_T) or 2:4 compressed
+// along M (OP_TSP); B is [K x N] dense.
+template <int AMODE>
+hipError_t gemm_tt_f32(const uint16_t* A, int64_t lda, const uint8_t* Am, int64_t ldam, const uint16_t* B,
+                       int64_t ldb, int64_t M, int64_t N, int64_t K, float* part, float* out, int64_t rows_out,
+                       bool transpose, int64_t ldo, hipStream_t st) {
+  if (K == 0) return hipSuccess;
+  const SplitPlan p = plan_splits(M, N, K);
+  GemmArgs g{};
+  g.A = A; g.lda = lda; g.Am = Am; g.ldam = ldam; g.B = B; g.ldb = ldb;
+  g.M = M; g.N = N; g.K = K; g.m_valid = M; g.ka_valid = K; g.kb_valid = K;
+  g.k_split = p.k_split; g.C = part; g.ldc = N;
+  hipError_t e = launch<CfgTT<AMODE>>(g, p.splits, st);
+  if (e != hipSuccess) return e;
+  const int64_t n_out = rows_out * N;
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)cdiv(n_out, 256)), dim3(256), 0, st, part, p.splits,
+                     M, N, rows_out, transpose ? 1 : 0, out, ldo);
+  return hipGetLastError();
+}
+
+struct FwdWs {
+  uint16_t *U_upT, *V_upT, *U_downT, *V_downT;
+  size_t bytes;
+};
+FwdWs fwd_ws(char* p, int64_t d, int64_t F, int64_t r) {
+  const int64_t Fp = pad64(F);
+  Carver c{p};
+  FwdWs w;
+  w.U_upT = c.take<uint16_t>(r * d);
+  w.V_upT = c.take<uint16_t>(Fp * r);
+  w.U_downT = c.take<uint16_t>(r * Fp);
+  w.V_downT = c.take<uint16_t>(d * r);
+  w.bytes = c.used;
+  return w;
+}
+
+struct BwdWs {
+  uint16_t *dZ, *dH, *dP;
+  float* part;
+  size_t bytes;
+};
+BwdWs bwd_ws(char* p, int64_t T, int64_t d, int64_t F, int64_t r) {
+  const int64_t Fp = pad64(F);
+  Carver c{p};
+  BwdWs w;
+  w.dZ = c.take<uint16_t>(T * r);
+  w.dH = c.take<uint16_t>(T * vals_ld(F));
+  w.dP = c.take<uint16_t>(T * r);
+  size_t pb = partial_bytes(r, d, T);
+  const size_t p2 = partial_bytes(Fp, r, T), p3 = partial_bytes(d, r, T);
+  if (p2 > pb) pb = p2;
+  if (p3 > pb) pb = p3;
+  w.part = c.take<float>(pb / sizeof(float));
+  w.bytes = c.used;
+  return w;
+}
+
+#define ELAS_TRY(...)                        \
+  do {                                       \
+    hipError_t e_ = (__VA_ARGS__);           \
+    if (e_ != hipSuccess) return e_;         \
+  } while (0)
+
+}  // namespace
+
+size_t spmm_workspace_bytes(int64_t K, int64_t N, int b_layout) {
+  return b_layout == 0 ? align_up((size_t)K * N * sizeof(uint16_t)) : 0;
+}
+
+size_t fwd_workspace_bytes(int64_t T, int64_t d, int64_t F, int64_t r) {
+  (void)T;
+  return fwd_ws(nullptr, d, F, r).bytes;
+}
+
+size_t bwd_workspace_bytes(int64_t T, int64_t d, int64_t F, int64_t r) {
+  return bwd_ws(nullptr, T, d, F, r).bytes;
+}
+
+hipError_t run_spmm24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, int64_t K, const uint16_t* b,
+                      int64_t N, bool b_is_nk, uint16_t* c, void* ws, hipStream_t st) {
+  if (M == 0) return hipSuccess;
+  const uint16_t* bt = b;
+  int64_t ldb = K;
+  if (!b_is_nk) {   // B [K x N] -> B^T [N x K] in the workspace
+    uint16_t* t = (uint16_t*)ws;
+    ELAS_TRY(transpose_pad(b, K, N, N, t, N, K, K, st));
+    bt = t;
+  }
+  GemmArgs g{};
+  g.A = a_vals; g.lda = vals_ld(K); g.Am = a_meta; g.ldam = meta_ld(K);
+  g.B = bt; g.ldb = ldb;
+  g.M = M; g.N = N; g.K = pad64(K); g.m_valid = M; g.ka_valid = pad64(K); g.kb_valid = K;
+  g.C = c; g.ldc = N;
+  return launch<CfgSP>(g, 1, st);
+}
+
+hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
+  const int64_t T = a.T, d = a.d, F = a.F, r = a.r, Fp = pad64(F);
+  const FwdWs w = fwd_ws((char*)a.ws, d, F, r);
+  // Weight factors laid out K-contiguous for the MFMA operands.
+  ELAS_TRY(transpose_pad(a.U_up, d, r, r, w.U_upT, r, d, d, st));          // [r x d]
+  ELAS_TRY(transpose_pad(a.V_up, r, F, F, w.V_upT, Fp, r, r, st));         // [Fp x r], zero rows >= F
+  ELAS_TRY(transpose_pad(a.U_down, F, r, r, w.U_downT, r, Fp, Fp, st));    // [r x Fp], zero cols >= F
+  ELAS_TRY(transpose_pad(a.V_down, r, d, d, w.V_downT, d, r, r, st));      // [d x r]
+  // P = x U_up
+  ELAS_TRY(gemm_nt_bf16(a.x, d, w.U_upT, d, a.P, r, T, r, d, st));
+  // H^T = V_up^T P^T with ReLU^2 + 2:4 selection + compression in the epilogue
+  {
+    GemmArgs g{};
+    g.A = w.V_upT; g.lda = r; g.B = a.P; g.ldb = r;
+    g.M = Fp; g.N = T; g.K = r; g.m_valid = Fp; g.ka_valid = r; g.kb_valid = r;
+    g.sv = a.s_vals; g.sm = a.s_meta; g.ldv = vals_ld(F); g.ldm = meta_ld(F);
+    ELAS_TRY(launch<CfgNT<256, EPI_SPARSIFY, true>>(g, 1, st));
+  }
+  // Z = S U_down on the 2:4 operand
+  {
+    GemmArgs g{};
+    g.A = a.s_vals; g.lda = vals_ld(F); g.Am = a.s_meta; g.ldam = meta_ld(F);
+    g.B = w.U_downT; g.ldb = Fp;
+    g.M = T; g.N = r; g.K = Fp; g.m_valid = T; g.ka_valid = Fp; g.kb_valid = Fp;
+    g.C = a.Z; g.ldc = r;
+    ELAS_TRY(launch<CfgSP>(g, 1, st));
+  }
+  // Y = Z V_down
+  ELAS_TRY(gemm_nt_bf16(a.Z, r, w.V_downT, r, a.y, d, T, d, r, st));
+  return hipSuccess;
+}
+
+hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
+  const int64_t T = a.T, d = a.d, F = a.F, r = a.r, Fp = pad64(F);
+  const int64_t ldv = vals_ld(F), ldm = meta_ld(F);
+  if (T == 0) {
+    ELAS_TRY(fill_zero(a.dU_up, d * r, st));
+    ELAS_TRY(fill_zero(a.dV_up, r * F, st));
+    ELAS_TRY(fill_zero(a.dU_down, F * r, st));
+    ELAS_TRY(fill_zero(a.dV_down, r * d, st));
+    return hipSuccess;
+  }
+  const BwdWs w = bwd_ws((char*)a.ws, T, d, F, r);
+  // dZ = dY V_down^T   (V_down [r x d] is already the K-contiguous operand)
+  ELAS_TRY(gemm_nt_bf16(a.dy, d, a.V_down, d, w.dZ, r, T, r, d, st));
+  // dV_down = Z^T dY
+  ELAS_TRY(gemm_tt_f32<OP_T>(a.Z, r, nullptr, 0, a.dy, d, r, d, T, w.part, a.dV_down, r, false, d, st));
+  // dH = (dZ U_down^T) * mask * 2 relu(H), computed as dS^T = U_down dZ^T
+  {
+    GemmArgs g{};
+    g.A = a.U_down; g.lda = r; g.B = w.dZ; g.ldb = r;
+    g.M = Fp; g.N = T; g.K = r; g.m_valid = F; g.ka_valid = r; g.kb_valid = r;
+    g.sv = a.s_vals; g.sm = a.s_meta; g.ldv = ldv; g.ldm = ldm; g.dv = w.dH;
+    ELAS_TRY(launch<CfgNT<256, EPI_DH, true>>(g, 1, st));
+  }
+  // dU_down = S^T dZ from the compressed S
+  ELAS_TRY(gemm_tt_f32<OP_TSP>(a.s_vals, ldv, a.s_meta, ldm, w.dZ, r, Fp, r, T, w.part, a.dU_down, F, false, r,
+                               st));
+  // dP = dH V_up^T on the 2:4 operand (V_up [r x F] is already K-contiguous)
+  {
+    GemmArgs g{};
+    g.A = w.dH; g.lda = ldv; g.Am = a.s_meta; g.ldam = ldm;
+    g.B = a.V_up; g.ldb = F;
+    g.M = T; g.N = r; g.K = Fp; g.m_valid = T; g.ka_valid = Fp; g.kb_valid = F;
+    g.C = w.dP; g.ldc = r;
+    ELAS_TRY(launch<CfgSP>(g, 1, st));
+  }
+  // dV_up = P^T dH, computed as dV_up^T = dH^T P and written transposed
+  ELAS_TRY(gemm_tt_f32<OP_TSP>(w.dH, ldv, a.s_meta, ldm, a.P_in, r, Fp, r, T, w.part, a.dV_up, F, true, F, st));
+  // dU_up = x^T dP
+  ELAS_TRY(gemm_tt_f32<OP_T>(a.x, d, nullptr, 0, w.dP, r, d, r, T, w.part, a.dU_up, d, false, r, st));
+  // dx = dP U_up^T   (U_up [d x r] is already K-contiguous)
+  ELAS_TRY(gemm_nt_bf16(w.dP, r, a.U_up, r, a.dx, d, T, d, r, st));
+  return hipSuccess;
+}
+
+}  // namespace elas

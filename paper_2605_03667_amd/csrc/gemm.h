@@ -1,0 +1,484 @@
+// Tiled MFMA GEMM for gfx950 (CDNA4): C = A * B with bf16 operands and fp32
+// accumulation, one template covering every product of the ELAS low-rank FFN
+// (forward and backward).
+//
+// Tiling: a workgroup of 256 threads (4 wave64s, WAVES_M x WAVES_N) owns a
+// BM x BN tile of C.  The contraction runs in steps of BK (64 dense, or 128
+// dense = 64 kept values for the 2:4 operand).  Both operands are staged in
+// LDS in "K-contiguous rows": row r of a tile holds BK (or 128) contraction
+// elements as 16-byte chunks; chunk c of row r lives at chunk position
+// c ^ (r & 7), so the eight lanes that read one 16-byte chunk each from eight
+// consecutive rows hit eight different bank groups.  LDS is double-buffered;
+// the next step's global loads are issued into registers before the current
+// step's MFMAs and written to the other LDS buffer after them, so there is one
+// barrier per step.
+//
+// Operand modes:
+//   OP_K    operand stored [rows x K] row-major (K contiguous): 16-byte copies.
+//   OP_T    operand stored [K x rows] (rows contiguous): each thread loads an
+//           8x8 block (8 K-rows x 8 consecutive row elements), transposes it in
+//           registers and writes 8 K-contiguous chunks.
+//   OP_SP   (A only) 2:4 compressed along K: kept values [rows x K/2] plus
+//           metadata [rows x K/8]; consumed by v_smfmac_f32_32x32x32_bf16.
+//   OP_TSP  (A only) 2:4 compressed along the row dimension of a [K x rows]
+//           matrix (S^T or dH^T read from the compressed activation): each
+//           thread expands 8x8 blocks from kept values + metadata to dense,
+//           transposes and writes K-contiguous chunks.
+//
+// MFMA layouts (pinned on gfx950 by a probe against a CPU product):
+//   v_mfma_f32_32x32x16_bf16: lane l holds A[row l%32][k 8(l/32)..+8] and
+//     B[k 8(l/32)..+8][col l%32]; accumulator i of lane l is
+//     C[row 8(i/4) + 4(l/32) + i%4][col l%32].
+//   v_smfmac_f32_32x32x32_bf16: the 16 index bits of a lane (bits 16*ABID..)
+//     hold 2 bits per kept value in slot order; kept slot j of lane l is row
+//     l%32, hardware K position 16(q/2) + 8(l/32) + 4(q%2) + idx_j with
+//     q = j/2; B lane l holds hardware K 16(l/32)..+16 of column l%32.
+//     Permuting the memory K order so that lane half h owns memory groups
+//     4h..4h+3 of each 32-wide step makes its 8 kept values one contiguous
+//     16-byte chunk whose 16 index bits are the canonical metadata shifted by
+//     16h; B lane half c then takes memory K [8c, 8c+8) and [16+8c, 16+8c+8).
+#pragma once
+
+#include "device.h"
+
+namespace elas {
+
+enum OpMode { OP_K = 0, OP_T = 1, OP_SP = 2, OP_TSP = 3 };
+enum EpiMode { EPI_BF16 = 0, EPI_F32 = 1, EPI_SPARSIFY = 2, EPI_DH = 3 };
+
+struct GemmArgs {
+  const uint16_t* A;   // OP_K [M x K], OP_T [K x M], OP_SP vals [M x K/2], OP_TSP vals [K x M/2]
+  int64_t lda;         // element pitch of A (or of its kept values)
+  const uint8_t* Am;   // OP_SP / OP_TSP metadata
+  int64_t ldam;        // byte pitch of the metadata
+  const uint16_t* B;   // OP_K [N x K], OP_T [K x N]
+  int64_t ldb;
+  int64_t M, N, K;     // C is M x N; contraction length K (dense count)
+  int64_t m_valid;     // rows of A that exist in memory (rows >= m_valid read as 0)
+  int64_t ka_valid;    // contraction entries of A that exist (>= read as 0)
+  int64_t kb_valid;    // contraction entries of B that exist
+  int64_t k_split;     // contraction length per split (multiple of the K step)
+  void* C;             // EPI_BF16: bf16 [M x N] pitch ldc; EPI_F32: float [splits][M][N]
+  int64_t ldc;
+  // EPI_SPARSIFY / EPI_DH: C rows are features f (M), columns are tokens t (N).
+  uint16_t* sv;        // kept values of S [N x ldv]: written (SPARSIFY) / read (DH)
+  uint8_t* sm;         // metadata of S [N x ldm]
+  int64_t ldv, ldm;
+  uint16_t* dv;        // EPI_DH: kept values of dH [N x ldv], written
+  int tiles_m, tiles_n;
+};
+
+template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int AMODE_, int BMODE_, int EPI_, bool M_FAST_>
+struct GemmCfg {
+  static constexpr int BM = BM_, BN = BN_, WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
+  static constexpr int AMODE = AMODE_, BMODE = BMODE_, EPI = EPI_;
+  static constexpr bool M_FAST = M_FAST_;   // consecutive tiles walk M (true) or N (false)
+  static constexpr bool SPARSE = AMODE_ == OP_SP;
+  static constexpr int BK = SPARSE ? 128 : 64;         // dense contraction per step
+  static constexpr int A_ROWB = 128;                     // bytes per LDS row of A (64 values)
+  static constexpr int B_ROWB = SPARSE ? 256 : 128;      // bytes per LDS row of B
+  static constexpr int A_BYTES = BM * A_ROWB;
+  static constexpr int AM_BYTES = SPARSE ? BM * 16 : 0;
+  static constexpr int B_BYTES = BN * B_ROWB;
+  static constexpr int STAGE = A_BYTES + AM_BYTES + B_BYTES;
+  static constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
+  static constexpr int FM = TM / 32, FN = TN / 32;
+  static_assert(WAVES_M * WAVES_N == 4, "4 waves");
+  static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be a multiple of 32");
+};
+
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ (row & 7); }
+
+// ---- transposes of 8x8 bf16 blocks held as 8 rows of uint4 ----------------
+// in[i] holds row i (8 consecutive elements); out[j] receives column j (the 8
+// rows' element j), so out[j] is a K-contiguous chunk when rows are K.
+__device__ __forceinline__ void transpose8x8(const uint4 (&in)[8], uint4 (&out)[8]) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    uint32_t w[4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const uint32_t* a = (const uint32_t*)&in[2 * p];
+      const uint32_t* b = (const uint32_t*)&in[2 * p + 1];
+      const uint32_t x = a[j >> 1], y = b[j >> 1];
+      w[p] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
+    }
+    out[j] = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+// Expand 2 groups (4 kept values in 8 bytes + 2 codes in one byte) to 8 dense
+// bf16 values packed as a uint4.
+__device__ __forceinline__ uint4 expand2(uint2 kept, uint32_t codes) {
+  uint32_t d[4];
+#pragma unroll
+  for (int g = 0; g < 2; ++g) {
+    const uint32_t pair = g ? kept.y : kept.x;
+    const uint32_t code = (codes >> (4 * g)) & 0xFu;
+    const uint32_t i0 = code & 3u, i1 = code >> 2;
+    const uint32_t v0 = pair & 0xFFFFu, v1 = pair >> 16;
+    uint32_t e[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) e[s] = (i0 == (uint32_t)s ? v0 : 0u) | (i1 == (uint32_t)s ? v1 : 0u);
+    d[2 * g] = e[0] | (e[1] << 16);
+    d[2 * g + 1] = e[2] | (e[3] << 16);
+  }
+  return make_uint4(d[0], d[1], d[2], d[3]);
+}
+
+// ---- operand staging --------------------------------------------------------
+// Registers that carry one K step of an operand from global memory to LDS.
+template <int ROWS, int ROWB, int MODE>
+struct Stager {
+  // OP_K / OP_SP: ROWS*ROWB/16 chunks of 16 bytes, CH per thread.
+  static constexpr int CHUNKS_PER_ROW = ROWB / 16;
+  static constexpr int CH = (MODE == OP_K || MODE == OP_SP) ? ROWS * CHUNKS_PER_ROW / 256 : 1;
+  // OP_T / OP_TSP: (BK/8) x (ROWS/8) blocks of 8x8, NB per thread (BK = 64).
+  static constexpr int NB = (MODE == OP_T || MODE == OP_TSP) ? (64 / 8) * (ROWS / 8) / 256 : 1;
+  static_assert(MODE == OP_T || MODE == OP_TSP || (ROWS * CHUNKS_PER_ROW) % 256 == 0, "chunks");
+  static_assert(!(MODE == OP_T || MODE == OP_TSP) || ((64 / 8) * (ROWS / 8)) % 256 == 0, "blocks");
+  uint4 r[(MODE == OP_T || MODE == OP_TSP) ? 8 * NB : CH];
+
+  // Global loads of the step starting at contraction index k0.
+  //   p, ld:      operand base and element pitch;
+  //   row0:       first tile row; rows_valid: rows that exist;
+  //   k_valid:    contraction entries that exist (dense count).
+  __device__ __forceinline__ void load(const uint16_t* __restrict__ p, int64_t ld, const uint8_t* __restrict__ pm,
+                                       int64_t ldm, int64_t row0, int64_t rows_valid, int64_t k0,
+                                       int64_t k_valid, int tid) {
+    if constexpr (MODE == OP_K || MODE == OP_SP) {
+      // OP_SP rows hold kept values: a 16-byte chunk is 8 values = 16 dense K.
+      constexpr int KPC = MODE == OP_SP ? 16 : 8;   // dense K per chunk
+#pragma unroll
+      for (int i = 0; i < CH; ++i) {
+        const int q = i * 256 + tid;
+        const int row = q / CHUNKS_PER_ROW, c = q % CHUNKS_PER_ROW;
+        const int64_t grow = row0 + row;
+        const int64_t gk = k0 + (int64_t)c * KPC;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (grow < rows_valid && gk < k_valid) {
+          const uint16_t* src = p + grow * ld + (MODE == OP_SP ? gk / 2 : gk);
+          v = *(const uint4*)src;
+        }
+        r[i] = v;
+      }
+    } else {
+      // 8x8 blocks: block b -> (kb, rb) with rb fastest so a wave's lanes read
+      // consecutive 16-byte pieces of the same K-row.
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int u = b * 256 + tid;
+        const int rb = u % (ROWS / 8), kb = u / (ROWS / 8);
+        const int64_t grow = row0 + rb * 8;
+        const bool rok = grow < rows_valid;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int64_t gk = k0 + kb * 8 + i;
+          uint4 v = make_uint4(0u, 0u, 0u, 0u);
+          if (rok && gk < k_valid) {
+            if constexpr (MODE == OP_T) {
+              v = *(const uint4*)(p + gk * ld + grow);
+            } else {
+              const uint2 kept = *(const uint2*)(p + gk * ld + grow / 2);
+              const uint32_t codes = pm[gk * ldm + grow / 8];
+              v = expand2(kept, codes);
+            }
+          }
+          r[8 * b + i] = v;
+        }
+      }
+    }
+  }
+
+  __device__ __forceinline__ void store(char* lds, int tid) const {
+    if constexpr (MODE == OP_K || MODE == OP_SP) {
+#pragma unroll
+      for (int i = 0; i < CH; ++i) {
+        const int q = i * 256 + tid;
+        const int row = q / CHUNKS_PER_ROW, c = q % CHUNKS_PER_ROW;
+        *(uint4*)(lds + row * ROWB + swz(row, c) * 16) = r[i];
+      }
+    } else {
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int u = b * 256 + tid;
+        const int rb = u % (ROWS / 8), kb = u / (ROWS / 8);
+        uint4 in[8], out[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) in[i] = r[8 * b + i];
+        transpose8x8(in, out);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int row = rb * 8 + j;
+          *(uint4*)(lds + row * ROWB + swz(row, kb) * 16) = out[j];
+        }
+      }
+    }
+  }
+};
+
+// Metadata rows of a 2:4 A tile: BM rows x 16 bytes (128 dense K).
+template <int BM>
+struct MetaStager {
+  static constexpr int CH = BM * 16 / 16 / 256 > 0 ? BM / 256 : 1;
+  uint4 r;
+  __device__ __forceinline__ void load(const uint8_t* __restrict__ pm, int64_t ldm, int64_t row0,
+                                       int64_t rows_valid, int64_t k0, int64_t k_valid, int tid) {
+    r = make_uint4(0u, 0u, 0u, 0u);
+    if (tid < BM) {
+      const int64_t grow = row0 + tid;
+      if (grow < rows_valid) {
+        const uint8_t* src = pm + grow * ldm + k0 / 8;
+        // 8 bytes cover 64 dense K; the row's metadata ends at k_valid / 8.
+        if (k0 + 64 <= k_valid) {
+          const uint2 lo = *(const uint2*)src;
+          r.x = lo.x; r.y = lo.y;
+        }
+        if (k0 + 128 <= k_valid) {
+          const uint2 hi = *(const uint2*)(src + 8);
+          r.z = hi.x; r.w = hi.y;
+        }
+      }
+    }
+  }
+  __device__ __forceinline__ void store(char* lds, int tid) const {
+    if (tid < BM) *(uint4*)(lds + tid * 16) = r;
+  }
+};
+
+// XCD-aware placement: consecutive workgroup ids go to different XCDs (8 on
+// MI355X), so remap them so that each XCD receives a contiguous range of
+// logical tiles, which then share operand rows in that XCD's L2.
+__device__ __forceinline__ int xcd_remap(int pid, int total) {
+  constexpr int kXcd = 8;
+  const int full = total / kXcd * kXcd;
+  if (pid >= full) return pid;
+  return (pid % kXcd) * (full / kXcd) + pid / kXcd;
+}
+
+template <class Cfg>
+__global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs g) {
+  constexpr int BM = Cfg::BM, BN = Cfg::BN, BK = Cfg::BK;
+  constexpr int FM = Cfg::FM, FN = Cfg::FN, TM = Cfg::TM, TN = Cfg::TN;
+  constexpr bool SPARSE = Cfg::SPARSE;
+  __shared__ __attribute__((aligned(16))) char smem[2 * Cfg::STAGE];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / Cfg::WAVES_N, wn = wave % Cfg::WAVES_N;
+  const int ntiles = g.tiles_m * g.tiles_n;
+  const int tile = xcd_remap(blockIdx.x, ntiles);
+  const int tm = Cfg::M_FAST ? tile % g.tiles_m : tile / g.tiles_n;
+  const int tn = Cfg::M_FAST ? tile / g.tiles_m : tile % g.tiles_n;
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+  const int64_t kbeg = (int64_t)blockIdx.y * g.k_split;
+  const int64_t kend = kbeg + g.k_split < g.K ? kbeg + g.k_split : g.K;
+  const int nsteps = (int)((kend - kbeg + BK - 1) / BK);
+
+  using SA = Stager<BM, Cfg::A_ROWB, Cfg::AMODE>;
+  using SB = Stager<BN, Cfg::B_ROWB, Cfg::BMODE>;
+  SA sa;
+  SB sb;
+  MetaStager<BM> sm;
+
+  auto load_step = [&](int64_t k0) {
+    sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, k0, g.ka_valid, tid);
+    if constexpr (SPARSE) sm.load(g.Am, g.ldam, m0, g.m_valid, k0, g.ka_valid, tid);
+    sb.load(g.B, g.ldb, nullptr, 0, n0, g.N, k0, g.kb_valid, tid);
+  };
+  auto store_step = [&](int buf) {
+    char* base = smem + buf * Cfg::STAGE;
+    sa.store(base, tid);
+    if constexpr (SPARSE) sm.store(base + Cfg::A_BYTES, tid);
+    sb.store(base + Cfg::A_BYTES + Cfg::AM_BYTES, tid);
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int lrow = lane & 31, lhalf = lane >> 5;
+
+  if (nsteps > 0) {
+    load_step(kbeg);
+    store_step(0);
+    __syncthreads();
+  }
+  for (int s = 0; s < nsteps; ++s) {
+    const int buf = s & 1;
+    if (s + 1 < nsteps) load_step(kbeg + (int64_t)(s + 1) * BK);
+    const char* lA = smem + buf * Cfg::STAGE;
+    const char* lM = lA + Cfg::A_BYTES;
+    const char* lB = lM + Cfg::AM_BYTES;
+    if constexpr (!SPARSE) {
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {       // four k16 MFMA steps per 64-wide K step
+        bf16x8 af[FM], bfr[FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+          const int row = wm * TM + i * 32 + lrow;
+          af[i] = *(const bf16x8*)(lA + row * 128 + swz(row, 2 * kk + lhalf) * 16);
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int row = wn * TN + j * 32 + lrow;
+          bfr[j] = *(const bf16x8*)(lB + row * 128 + swz(row, 2 * kk + lhalf) * 16);
+        }
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+      }
+    } else {
+      uint4 meta[FM];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const int row = wm * TM + i * 32 + lrow;
+        meta[i] = *(const uint4*)(lM + row * 16);
+      }
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {       // four 32-wide smfmac steps per 128-wide K step
+        bf16x8 af[FM];
+        bf16x16 bfr[FN];
+        int idx[FM];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+          const int row = wm * TM + i * 32 + lrow;
+          af[i] = *(const bf16x8*)(lA + row * 128 + swz(row, 2 * kk + lhalf) * 16);
+          const uint32_t w = kk == 0 ? meta[i].x : kk == 1 ? meta[i].y : kk == 2 ? meta[i].z : meta[i].w;
+          idx[i] = (int)(w >> (16 * lhalf));
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int row = wn * TN + j * 32 + lrow;
+          const bf16x8 lo = *(const bf16x8*)(lB + row * 256 + swz(row, 4 * kk + lhalf) * 16);
+          const bf16x8 hi = *(const bf16x8*)(lB + row * 256 + swz(row, 4 * kk + 2 + lhalf) * 16);
+          bfr[j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
+        }
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_smfmac_f32_32x32x32_bf16(af[i], bfr[j], acc[i][j], idx[i], 0, 0);
+      }
+    }
+    if (s + 1 < nsteps) store_step(buf ^ 1);
+    __syncthreads();
+  }
+
+  // ---------------------------------------------------------------- epilogues
+  if constexpr (Cfg::EPI == EPI_BF16 || Cfg::EPI == EPI_F32) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int64_t col = n0 + wn * TN + j * 32 + lrow;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int64_t row = m0 + wm * TM + i * 32 + (e / 4) * 8 + lhalf * 4 + (e % 4);
+          if (row < g.M && col < g.N) {
+            if constexpr (Cfg::EPI == EPI_BF16) {
+              const __bf16 v = (__bf16)acc[i][j][e];
+              ((__bf16*)g.C)[row * g.ldc + col] = v;
+            } else {
+              float* part = (float*)g.C + (int64_t)blockIdx.y * g.M * g.N;
+              part[row * g.N + col] = acc[i][j][e];
+            }
+          }
+        }
+      }
+  } else {
+    // C rows are features f, columns tokens t.  Accumulators 4b..4b+3 of a
+    // lane are features 8b + 4h + 0..3 of a 32-row block: one whole group of
+    // 4 (Algorithm 1).  Lanes l and l+32 hold the even and odd groups of the
+    // same 8 features, i.e. the two nibbles of one metadata byte.
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int64_t t = n0 + wn * TN + j * 32 + lrow;
+        const int64_t f32 = m0 + wm * TM + i * 32;     // first feature of the 32-row block
+        uint32_t pair[4], codes = 0;
+        if constexpr (Cfg::EPI == EPI_SPARSIFY) {
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            uint32_t r[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const __bf16 hb = (__bf16)acc[i][j][4 * b + q];      // h rounded to bf16 (RNE)
+              r[q] = relu_bits(__builtin_bit_cast(uint16_t, hb));
+            }
+            const uint32_t code = top2_code(r[0], r[1], r[2], r[3]);
+            const uint32_t kept = pick_pair(code, r[0], r[1], r[2], r[3]);
+            const float a = bf16_to_f32(kept & 0xFFFFu), c = bf16_to_f32(kept >> 16);
+            pair[b] = f32_to_bf16_rne(a * a) | (f32_to_bf16_rne(c * c) << 16);
+            codes |= code << (4 * b);
+          }
+        } else {
+          // EPI_DH: read the stored group (values + code) and scale dS at the
+          // kept positions by 2 relu(h), relu(h) = bf16(sqrt(s)) exactly.
+          uint32_t sv[4] = {0u, 0u, 0u, 0u};
+          uint32_t word = 0;
+          if (t < g.N && f32 < g.M) {
+            // this lane's groups: 8b + 4h -> group index (f32/4) + 2b + h
+            word = *(const uint32_t*)(g.sm + t * g.ldm + f32 / 8);
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+              sv[b] = *(const uint32_t*)(g.sv + t * g.ldv + (f32 / 4 + 2 * b + lhalf) * 2);
+          }
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const uint32_t code = (word >> (8 * b + 4 * lhalf)) & 0xFu;
+            const uint32_t i0 = code & 3u, i1 = code >> 2;
+            float ds[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) ds[q] = acc[i][j][4 * b + q];
+            const float d0 = i0 == 0u ? ds[0] : i0 == 1u ? ds[1] : ds[2];
+            const float d1 = i1 == 1u ? ds[1] : i1 == 2u ? ds[2] : ds[3];
+            const float s0 = bf16_to_f32(sv[b] & 0xFFFFu), s1 = bf16_to_f32(sv[b] >> 16);
+            const float r0 = (float)(__bf16)__builtin_sqrtf(s0);
+            const float r1 = (float)(__bf16)__builtin_sqrtf(s1);
+            const uint32_t o0 = __builtin_bit_cast(uint16_t, (__bf16)(d0 * 2.0f * r0));
+            const uint32_t o1 = __builtin_bit_cast(uint16_t, (__bf16)(d1 * 2.0f * r1));
+            pair[b] = o0 | (o1 << 16);
+            codes |= code << (4 * b);
+          }
+        }
+        // Lane pair (l, l+32) -> one 32-bit metadata word and 16 kept values
+        // (groups f32/4 .. f32/4+7).  Lane half 0 writes groups 0..3, half 1
+        // groups 4..7, 16 bytes each.
+        const uint32_t other_codes = __shfl_xor(codes, 32);
+        uint32_t give0 = lhalf ? pair[0] : pair[2];
+        uint32_t give1 = lhalf ? pair[1] : pair[3];
+        const uint32_t got0 = __shfl_xor(give0, 32);
+        const uint32_t got1 = __shfl_xor(give1, 32);
+        if (t < g.N && f32 < g.M) {
+          // groups in order: half 0 owns even groups (b -> 2b), half 1 odd (2b+1)
+          uint4 out;
+          if (lhalf == 0) {   // groups 0,1,2,3 = mine b0, other b0, mine b1, other b1
+            out = make_uint4(pair[0], got0, pair[1], got1);
+          } else {            // groups 4,5,6,7 = other b2, mine b2, other b3, mine b3
+            out = make_uint4(got0, pair[2], got1, pair[3]);
+          }
+          uint16_t* dst = (Cfg::EPI == EPI_SPARSIFY ? g.sv : g.dv) + t * g.ldv + f32 / 2 + lhalf * 8;
+          *(uint4*)dst = out;
+          if constexpr (Cfg::EPI == EPI_SPARSIFY) {
+            if (lhalf == 0) {
+              uint32_t word = 0;
+#pragma unroll
+              for (int b = 0; b < 4; ++b)
+                word |= (((codes >> (4 * b)) & 0xFu) | (((other_codes >> (4 * b)) & 0xFu) << 4)) << (8 * b);
+              *(uint32_t*)(g.sm + t * g.ldm + f32 / 8) = word;
+            }
+          }
+        }
+      }
+  }
+}
+
+}  // namespace elas

@@ -1,0 +1,75 @@
+"""Shared test utilities: bf16 bit arrays <-> torch tensors, the padded
+compressed layout, and the comparison protocol between the GPU path and the
+oracle.  Holds none of the method's arithmetic."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+
+def dev_bf16(bits: np.ndarray) -> torch.Tensor:
+    """uint16 bf16 bit array -> bf16 tensor on cuda:0."""
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to("cuda:0")
+
+
+def host_bits(t: torch.Tensor) -> np.ndarray:
+    """bf16 tensor -> uint16 bit array on the host."""
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def vals_ld(N: int) -> int:
+    return 32 * ((N + 63) // 64)
+
+
+def meta_ld(N: int) -> int:
+    return 8 * ((N + 63) // 64)
+
+
+def pad_compressed(vals: np.ndarray, meta: np.ndarray, N: int):
+    """Canonical (vals [M, N/2], meta [M, N/8]) -> the library's padded rows:
+    padding groups hold zeros and code 0x4 (positions 0 and 1)."""
+    M = vals.shape[0]
+    v = np.zeros((M, vals_ld(N)), dtype=vals.dtype)
+    v[:, : N // 2] = vals
+    m = np.full((M, meta_ld(N)), 0x44, dtype=np.uint8)
+    m[:, : N // 8] = meta
+    return v, m
+
+
+def check_padding(vals: np.ndarray, meta: np.ndarray, N: int):
+    """The padding of the library's compressed rows holds zeros / code 0x4."""
+    assert np.all(vals[:, N // 2:] == 0), "padding values must be zero"
+    assert np.all(meta[:, N // 8:] == 0x44), "padding codes must be 0x4"
+
+
+def rel_fro(a, b) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    nb = np.linalg.norm(b)
+    if nb == 0:
+        return float(np.linalg.norm(a))
+    return float(np.linalg.norm(a - b) / nb)
+
+
+def mask_gate(gpu_mask: np.ndarray, ref_mask: np.ndarray, ref_keys: np.ndarray, rel: float = 1e-2):
+    """Mask-disagreement rule: in every group where the two masks differ, each
+    entry kept only by the GPU and each entry kept only by the oracle must have
+    oracle keys within rel * max(key_e, key_f, mean key) of each other.
+    Returns (number of groups that differ, number that break the rule)."""
+    M, N = ref_mask.shape
+    g = gpu_mask.reshape(M, N // 4, 4)
+    o = ref_mask.reshape(M, N // 4, 4)
+    k = ref_keys.reshape(M, N // 4, 4)
+    diff = np.any(g != o, axis=-1)
+    idx = np.argwhere(diff)
+    floor = float(ref_keys.mean())
+    bad = 0
+    for i, j in idx:
+        only_gpu = np.nonzero(g[i, j] & ~o[i, j])[0]
+        only_ref = np.nonzero(o[i, j] & ~g[i, j])[0]
+        for e in only_gpu:
+            for f in only_ref:
+                ke, kf = k[i, j, e], k[i, j, f]
+                if abs(kf - ke) > rel * max(ke, kf, floor):
+                    bad += 1
+    return int(diff.sum()), bad

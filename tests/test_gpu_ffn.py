@@ -1,0 +1,187 @@
+"""End-to-end parity of elas_lowrank_ffn_fwd / elas_lowrank_ffn_bwd with the
+oracle (bf16 inputs, fp32 accumulation).
+
+* Mask gate: wherever the GPU's 2:4 mask differs from the oracle's, the
+  competing ReLU^2 magnitudes differ by less than 1e-2 relative (floored at
+  the mean magnitude).
+* Numeric gate: relative Frobenius error <= 2e-2 for Y, dx and the four
+  weight gradients against the oracle with the same bf16 rounding points.
+* With exact small-integer inputs the fused ReLU^2 + 2:4 epilogue must
+  match the oracle bit for bit (P, kept values, metadata).
+* Full-size workloads run in the benchmarked configuration and are checked
+  on sampled tokens: every output row depends only on its own token, and the
+  weight gradients are checked with dY zero outside the sampled tokens, so
+  that they are exact sums over those tokens.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2605_03667_amd as elas
+from oracle import bf16 as obf
+from oracle import ffn as offn
+from oracle import sparsify as osp
+from synthetic import CONFIGS, config_inputs, ffn_inputs, uniform_int_bf16
+from tests.helpers import check_padding, dev_bf16, host_bits, mask_gate, rel_fro
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+GRADS = ("dU_up", "dV_up", "dU_down", "dV_down")
+
+
+def run_gpu(bits, rows=None):
+    """Forward + backward through the C ABI; returns host copies (float64 for
+    numbers) of the outputs, restricted to the token rows ``rows`` if given."""
+    t = {k: dev_bf16(v) for k, v in bits.items()}
+    fwd = elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"])
+    bwd = elas.elas_lowrank_ffn_bwd(t["dY"], t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], fwd)
+    torch.cuda.synchronize()
+    del t
+    F = bits["V_up"].shape[1]
+    idx = None if rows is None else torch.as_tensor(rows, device="cuda:0")
+
+    def rows_of(x):
+        return x if idx is None else x.index_select(0, idx)
+
+    out = {
+        "Y": obf.to_f64(host_bits(rows_of(fwd["y"]))), "P": obf.to_f64(host_bits(rows_of(fwd["P"]))),
+        "Z": obf.to_f64(host_bits(rows_of(fwd["Z"]))), "dx": obf.to_f64(host_bits(rows_of(bwd["dx"]))),
+        "s_vals": host_bits(rows_of(fwd["s_vals"])), "s_meta": rows_of(fwd["s_meta"]).cpu().numpy(),
+    }
+    for k in GRADS:
+        out[k] = bwd[k].cpu().numpy().astype(np.float64)
+    del fwd, bwd
+    check_padding(out["s_vals"], out["s_meta"], F)
+    dense, mask = osp.decompress(out["s_vals"][:, : F // 2], out["s_meta"][:, : F // 8], F)
+    out["mask"] = mask
+    out["S"] = obf.to_f64(dense)
+    return out
+
+
+def compare(gpu, f, b, grads=True, report=None):
+    """Mask gate and numeric gate (gpu and oracle hold the same token rows)."""
+    flips, bad = mask_gate(gpu["mask"], f["mask"], f["s"])
+    assert bad == 0, f"{bad} mask disagreements outside the 1e-2 window ({flips} groups differ)"
+    errs = {"Y": rel_fro(gpu["Y"], f["Y"]), "dx": rel_fro(gpu["dx"], b["dx"]),
+            "P": rel_fro(gpu["P"], f["P"]), "Z": rel_fro(gpu["Z"], f["Z"])}
+    if grads:
+        for k in GRADS:
+            errs[k] = rel_fro(gpu[k], b[k])
+    if report is not None:
+        report.update(errs, flips=flips, groups=f["mask"].size // 4)
+    for k, e in errs.items():
+        assert e <= TOL, (k, e, errs)
+    return errs
+
+
+@pytest.mark.parametrize("T,d,F,r", [(5, 16, 24, 8), (1, 64, 64, 16), (700, 136, 1000, 72),
+                                     (256, 256, 256, 256), (300, 512, 1376, 128), (129, 768, 2048, 256)])
+def test_small_shapes(T, d, F, r):
+    bits = ffn_inputs(T, d, F, r, seed_base=T + d)
+    f, b = offn.run(bits)
+    compare(run_gpu(bits), f, b)
+
+
+@pytest.mark.parametrize("cfg", ["llama60m"])
+def test_llama60m_full(cfg):
+    bits = config_inputs(cfg)
+    f, b = offn.run(bits)
+    rep = {}
+    compare(run_gpu(bits), f, b, report=rep)
+    print(cfg, rep)
+
+
+@pytest.mark.parametrize("cfg", ["llama130m", "llama350m", "llama1b"])
+def test_model_shapes_reduced_tokens(cfg):
+    bits = config_inputs(cfg, T=1024)
+    f, b = offn.run(bits)
+    rep = {}
+    compare(run_gpu(bits), f, b, report=rep)
+    print(cfg, rep)
+
+
+def test_exact_fused_epilogue():
+    """Small integers: P = x U_up and H = P V_up are exact in fp32 and float64
+    and P fits bf16, so bf16(H), the 2:4 selection, the kept ReLU^2 values and
+    the metadata are identical on both sides."""
+    T, d, F, r = 700, 64, 1000, 40
+    bits = {
+        "x": uniform_int_bf16((T, d), -1, 1, 1), "U_up": uniform_int_bf16((d, r), -1, 1, 2),
+        "V_up": uniform_int_bf16((r, F), -1, 1, 3), "U_down": uniform_int_bf16((F, r), -1, 1, 4, -12),
+        "V_down": uniform_int_bf16((r, d), -1, 1, 5, -4), "dY": uniform_int_bf16((T, d), -1, 1, 6),
+    }
+    f, b = offn.run(bits)
+    gpu = run_gpu(bits)
+    np.testing.assert_array_equal(gpu["P"], f["P"])
+    ref_vals, ref_meta = osp.compress(obf.from_f64(f["S"]), f["mask"])
+    np.testing.assert_array_equal(gpu["s_meta"][:, : F // 8], ref_meta)
+    np.testing.assert_array_equal(gpu["s_vals"][:, : F // 2], ref_vals)
+    compare(gpu, f, b)
+
+
+def test_all_h_nonpositive_gives_exact_zeros():
+    T, d, F, r = 300, 64, 136, 24
+    bits = ffn_inputs(T, d, F, r, seed_base=5)
+    bits["x"] = bits["x"] & np.uint16(0x7FFF)
+    bits["U_up"] = bits["U_up"] & np.uint16(0x7FFF)
+    bits["V_up"] = bits["V_up"] | np.uint16(0x8000)
+    gpu = run_gpu(bits)
+    assert np.all(gpu["Y"] == 0) and np.all(gpu["dx"] == 0)
+    for k in GRADS:
+        assert np.all(gpu[k] == 0), k
+
+
+def test_deterministic():
+    bits = ffn_inputs(700, 136, 1000, 72, seed_base=3)
+    a, b = run_gpu(bits), run_gpu(bits)
+    for k in ("Y", "dx", "s_vals", "s_meta") + GRADS:
+        np.testing.assert_array_equal(a[k], b[k], err_msg=k)
+
+
+def _sample_rows(T, n, seed):
+    g = np.random.default_rng(seed)
+    return np.unique(np.concatenate([[0, T - 1], g.integers(0, T, n)]))
+
+
+@pytest.mark.parametrize("cfg", ["llama130m", "llama350m", "llama1b", "llama1b_t262144"])
+def test_full_size_sampled(cfg):
+    bits = config_inputs(cfg)
+    T = CONFIGS[cfg]["T"]
+    rows = _sample_rows(T, 94, 1)
+    # outputs per token: y, dx, saved P and Z, the mask
+    sub = {k: (v[rows] if k in ("x", "dY") else v) for k, v in bits.items()}
+    f, b = offn.run(sub)
+    gpu = run_gpu(bits, rows)
+    rep = {}
+    compare(gpu, f, b, grads=False, report=rep)
+    del gpu
+    # weight gradients: dY zero outside the sampled tokens
+    dY = np.zeros_like(bits["dY"])
+    dY[rows] = bits["dY"][rows]
+    bits["dY"] = dY
+    gpu = run_gpu(bits, rows)
+    sub["dY"] = dY[rows]
+    f, b = offn.run(sub)
+    for k in GRADS:
+        e = rel_fro(gpu[k], b[k])
+        rep[k] = e
+        assert e <= TOL, (k, e)
+    print(cfg, rep)
+
+
+def test_zero_tokens():
+    """T = 0: the forward is a no-op and the backward writes zero weight
+    gradients (over whatever the buffers held)."""
+    d, F, r = 64, 136, 24
+    bits = ffn_inputs(0, d, F, r, seed_base=9)
+    t = {k: dev_bf16(v) for k, v in bits.items()}
+    fwd = elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"])
+    grads = {"dx": torch.empty((0, d), dtype=torch.bfloat16, device="cuda:0")}
+    for k, shp in (("dU_up", (d, r)), ("dV_up", (r, F)), ("dU_down", (F, r)), ("dV_down", (r, d))):
+        grads[k] = torch.full(shp, float("nan"), dtype=torch.float32, device="cuda:0")
+    elas.elas_lowrank_ffn_bwd(t["dY"], t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], fwd,
+                              grads=grads)
+    torch.cuda.synchronize()
+    for k in GRADS:
+        assert torch.all(grads[k] == 0), k
