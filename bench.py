@@ -1,0 +1,227 @@
+"""Benchmark of the ELAS low-rank 2:4 FFN (forward + backward) on one MI355X.
+
+One step = elas_lowrank_ffn_fwd + elas_lowrank_ffn_bwd over one batch of the
+LLaMA-1B-shape FFN layer (T = 65536 tokens, d = 2048, d_ff = 5464 (5461 padded),
+r = 512), seeded synthetic bf16 inputs resident in HBM.  Prints one JSON line.
+
+Besides tokens/s it reports, from per-kernel HIP events recorded by the
+library on the launch stream during the timed steps:
+  roofline  -- the kernel with the largest share of the step: algorithmic
+               FLOP per launch / average launch time vs the bf16 MFMA peak;
+  spgemm    -- the 2:4 sparse x dense down projection (v_smfmac);
+  kernels   -- every kernel's launches, average time and rate;
+and, timed separately, the standalone sparsify kernel on h [65536 x 2736]
+(the 350M-shape activation) against the HBM peak, plus the CPU oracle on a
+bounded sample of the same workload (cpu_baseline).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "low-rank FFN fwd+bwd tokens/s at 1B shape; 2:4 SpGEMM TFLOP/s vs MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def algorithmic_flops(tag: str, T: int, d: int, F: int, r: int) -> float | None:
+    """Algorithmic FLOP of one launch of a kernel tag (T tokens per launch).
+
+    Dense products count 2 FLOP per multiply-add.  Products whose one side is
+    the 2:4 activation count only the kept half (T r F instead of 2 T r F),
+    including the masked dH product whose discarded half is still computed.
+    """
+    table = {
+        "k1_up_gemm": 2 * T * d * r, "k2_up_relu2_sparsify": 2 * T * r * F, "k3_spmm_down": T * r * F,
+        "k4_down_gemm": 2 * T * r * d, "b1_dZ": 2 * T * d * r, "b2_dV_down": 2 * T * d * r,
+        "b3_dH_masked": T * r * F, "b4_dU_down": T * r * F, "b5_spmm_dP": T * r * F, "b6_dV_up": T * r * F,
+        "b7_dU_up": 2 * T * d * r, "b8_dx": 2 * T * d * r,
+    }
+    v = table.get(tag)
+    return None if v is None else float(v)
+
+
+def executed_flops(tag: str, T: int, d: int, F: int, r: int) -> float | None:
+    """FLOP the kernel actually issues (dense-equivalent for smfmac)."""
+    a = algorithmic_flops(tag, T, d, F, r)
+    if a is None:
+        return None
+    Fp = 64 * ((F + 63) // 64)
+    if tag in ("k2_up_relu2_sparsify",):
+        return 2.0 * T * r * Fp
+    if tag in ("k3_spmm_down", "b3_dH_masked", "b4_dU_down", "b5_spmm_dP", "b6_dV_up"):
+        return 2.0 * T * r * Fp
+    return a
+
+
+def cpu_baseline(cfg: dict, sample_tokens: int) -> dict:
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import ffn as offn
+    from synthetic import config_inputs
+
+    bits = config_inputs("llama1b", T=sample_tokens)
+    t0 = time.perf_counter()
+    offn.run(bits)
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    return {"value": sample_tokens / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "seconds": dt,
+            "sample": f"{sample_tokens} tokens of the 1B-shape FFN workload (d={cfg['d']}, d_ff={cfg['d_ff']}, "
+                      f"r={cfg['r']}), float64 numpy oracle, forward + backward with bf16 rounding points"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama1b")
+    ap.add_argument("--cpu-sample", type=int, default=16384, help="tokens for the CPU oracle baseline (0: skip)")
+    ap.add_argument("--no-sparsify", action="store_true", help="skip the standalone sparsify measurement")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (--gpus {args.gpus} requested): the ELAS FFN path here is "
+              f"single-GPU; see DESIGN.md for how it would shard.", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2605_03667_amd as elas
+    from synthetic import CONFIGS, SPARSIFY_SHAPE, config_inputs, h_input
+
+    cfg = CONFIGS[args.workload]
+    T, d, F, r = cfg["T"], cfg["d"], cfg["d_ff"], cfg["r"]
+    dev = torch.device("cuda:0")
+    bits = config_inputs(args.workload)
+
+    def to_dev(b):
+        return torch.from_numpy(b.view(np.int16)).view(torch.bfloat16).to(dev)
+
+    t = {k: to_dev(v) for k, v in bits.items()}
+    del bits
+    bf, f32 = torch.bfloat16, torch.float32
+    out = {"y": torch.empty((T, d), dtype=bf, device=dev), "P": torch.empty((T, r), dtype=bf, device=dev),
+           "s_vals": torch.empty((T, elas.elas_vals_ld(F)), dtype=bf, device=dev),
+           "s_meta": torch.empty((T, elas.elas_meta_ld(F)), dtype=torch.uint8, device=dev),
+           "Z": torch.empty((T, r), dtype=bf, device=dev)}
+    grads = {"dx": torch.empty((T, d), dtype=bf, device=dev), "dU_up": torch.empty((d, r), dtype=f32, device=dev),
+             "dV_up": torch.empty((r, F), dtype=f32, device=dev), "dU_down": torch.empty((F, r), dtype=f32, device=dev),
+             "dV_down": torch.empty((r, d), dtype=f32, device=dev)}
+    ws_f = torch.empty(max(1, elas.elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r)), dtype=torch.uint8, device=dev)
+    ws_b = torch.empty(max(1, elas.elas_lowrank_ffn_bwd_workspace_bytes(T, d, F, r)), dtype=torch.uint8, device=dev)
+
+    def step():
+        elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], out=out, workspace=ws_f)
+        elas.elas_lowrank_ffn_bwd(t["dY"], t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], out,
+                                  grads=grads, workspace=ws_b)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+
+    # ---- timed region: K steps, per-kernel events recorded by the library ----
+    elas.elas_timing_enable(True)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    elas.elas_timing_enable(False)
+    total_ms = start.elapsed_time(stop)
+    kernels = elas.elas_timing_collect()
+    ms_per_step = total_ms / args.steps
+    tokens_per_s = T / (ms_per_step / 1e3)
+    print(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
+
+    # same steps without per-kernel events, for reference
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_plain = start.elapsed_time(stop) / args.steps
+
+    ktab = {}
+    for tag, (n, ms) in sorted(kernels.items(), key=lambda kv: -kv[1][1]):
+        avg_us = ms / n * 1e3
+        row = {"launches": n, "avg_us": round(avg_us, 2), "share": round(ms / total_ms, 4)}
+        a = algorithmic_flops(tag, T, d, F, r)
+        if a is not None:
+            row["alg_tflops"] = round(a / (avg_us * 1e-6) / 1e12, 1)
+            row["exec_tflops"] = round(executed_flops(tag, T, d, F, r) / (avg_us * 1e-6) / 1e12, 1)
+        ktab[tag] = row
+    gemm_tags = [k for k in ktab if algorithmic_flops(k, T, d, F, r) is not None]
+    dom = max(gemm_tags, key=lambda k: kernels[k][1])
+    dom_avg_s = kernels[dom][1] / kernels[dom][0] / 1e3
+    dom_alg = algorithmic_flops(dom, T, d, F, r)
+    achieved = dom_alg / dom_avg_s / 1e12
+    roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "alg_flop_per_launch": dom_alg, "avg_us": round(dom_avg_s * 1e6, 2)}
+
+    sp_tag = "k3_spmm_down"
+    sp_avg_s = kernels[sp_tag][1] / kernels[sp_tag][0] / 1e3
+    sp_alg = algorithmic_flops(sp_tag, T, d, F, r) / sp_avg_s / 1e12
+    spgemm = {"kernel": sp_tag, "avg_us": round(sp_avg_s * 1e6, 2), "alg_tflops": round(sp_alg, 1),
+              "dense_equiv_tflops": round(2 * sp_alg, 1), "frac_of_dense_bf16_peak": round(sp_alg / PEAK_BF16_TFLOPS, 4),
+              "frac_of_sparse_bf16_peak": round(2 * sp_alg / (2 * PEAK_BF16_TFLOPS), 4)}
+
+    result = {
+        "metric": METRIC, "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded Gaussian bf16 inputs, fan-in scaled weights)",
+        "config": {"workload": f"{args.workload}_ffn_fwd_bwd", "T": T, "d": d, "d_ff": F,
+                   "d_ff_true": cfg["d_ff_true"], "r": r},
+        "roofline": roofline, "spgemm": spgemm, "ms_per_step_no_kernel_events": round(ms_plain, 4),
+        "kernels": ktab,
+    }
+
+    # ---- standalone sparsify on h [65536 x 2736] -----------------------------
+    if not args.no_sparsify:
+        M, N = SPARSIFY_SHAPE
+        del out, grads, ws_f, ws_b, t
+        torch.cuda.empty_cache()
+        h = to_dev(h_input(M, N, seed=2))
+        vals = torch.empty((M, elas.elas_vals_ld(N)), dtype=bf, device=dev)
+        meta = torch.empty((M, elas.elas_meta_ld(N)), dtype=torch.uint8, device=dev)
+        for _ in range(3):
+            elas.elas_sparsify_24(h, vals=vals, meta=meta)
+        torch.cuda.synchronize()
+        elas.elas_timing_enable(True)
+        for _ in range(20):
+            elas.elas_sparsify_24(h, vals=vals, meta=meta)
+        torch.cuda.synchronize()
+        elas.elas_timing_enable(False)
+        n, ms = elas.elas_timing_collect()["sparsify24"]
+        avg_s = ms / n / 1e3
+        alg_bytes = M * N * (2 + 1.125)      # read bf16 h, write half the values + 2 bits each
+        gbs = alg_bytes / avg_s / 1e9
+        result["sparsify"] = {"shape": [M, N], "avg_us": round(avg_s * 1e6, 2), "alg_bytes": alg_bytes,
+                              "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                              "frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+    if args.cpu_sample > 0:
+        print(f"[bench] cpu oracle on {args.cpu_sample} tokens", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(cfg, args.cpu_sample)
+
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

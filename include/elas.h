@@ -172,6 +172,21 @@ int elas_lowrank_ffn_bwd(const uint16_t* dy, const uint16_t* x, const uint16_t* 
                          uint16_t* dx, float* dU_up, float* dV_up, float* dU_down, float* dV_down,
                          void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Per-kernel timing (diagnostics for benchmarks; not thread-safe).
+ *
+ * elas_timing_enable(1) clears earlier records and starts recording: every
+ * kernel the entry points launch is then bracketed by two hipEvents recorded
+ * on the caller's stream.  elas_timing_enable(0) stops recording.
+ * elas_timing_collect() waits for the recorded events and aggregates them per
+ * kernel tag; it returns the number of tags (or -ELAS_ERR_DEVICE).
+ * elas_timing_entry(i, ...) returns tag i's name (NUL-terminated, truncated to
+ * name_cap), its number of launches and their summed duration in ms.
+ */
+int elas_timing_enable(int enable);
+int elas_timing_collect(void);
+int elas_timing_entry(int i, char* name, int name_cap, int64_t* launches, double* total_ms);
+
 #ifdef __cplusplus
 }
 #endif

@@ -21,6 +21,7 @@ __all__ = [
     "ElasError", "lib", "elas_vals_ld", "elas_meta_ld", "elas_sparsify_24", "elas_spmm_24",
     "elas_spmm_24_workspace_bytes", "elas_lowrank_ffn_fwd", "elas_lowrank_ffn_fwd_workspace_bytes",
     "elas_lowrank_ffn_bwd", "elas_lowrank_ffn_bwd_workspace_bytes",
+    "elas_timing_enable", "elas_timing_collect",
     "ELAS_SPARSIFY_RELU2", "ELAS_SPARSIFY_RAW", "ELAS_B_KN", "ELAS_B_NK",
 ]
 
@@ -61,6 +62,10 @@ _SIGNATURES = {
     "elas_lowrank_ffn_bwd_workspace_bytes": ([_i64, _i64, _i64, _i64], _sz),
     "elas_lowrank_ffn_bwd": ([_p] * 6 + [_i64] * 4 + [_u32] + [_p] * 4 + [_p] * 5 + [_p, _sz, _p],
                              ctypes.c_int),
+    "elas_timing_enable": ([ctypes.c_int], ctypes.c_int),
+    "elas_timing_collect": ([], ctypes.c_int),
+    "elas_timing_entry": ([ctypes.c_int, ctypes.c_char_p, ctypes.c_int, ctypes.POINTER(_i64),
+                           ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
 }
 
 
@@ -219,3 +224,24 @@ def elas_lowrank_ffn_bwd(dy, x, U_up, V_up, U_down, V_down, saved: dict, flags: 
         _ptr(workspace, torch.uint8, "workspace"), 0 if workspace is None else workspace.numel(),
         _stream(dev)))
     return grads
+
+
+def elas_timing_enable(enable: bool = True) -> None:
+    """Start (clearing earlier records) or stop per-kernel event timing."""
+    _check(lib().elas_timing_enable(1 if enable else 0))
+
+
+def elas_timing_collect() -> dict:
+    """{kernel tag: (launches, total ms)} of the launches recorded so far."""
+    L = lib()
+    n = L.elas_timing_collect()
+    if n < 0:
+        _check(-n)
+    out = {}
+    buf = ctypes.create_string_buffer(128)
+    for i in range(n):
+        launches = _i64()
+        ms = ctypes.c_double()
+        _check(L.elas_timing_entry(i, buf, 128, ctypes.byref(launches), ctypes.byref(ms)))
+        out[buf.value.decode()] = (launches.value, ms.value)
+    return out

@@ -49,6 +49,7 @@ __global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __re
 hipError_t transpose_pad(const uint16_t* in, int64_t rows, int64_t cols, int64_t ldi, uint16_t* out,
                          int64_t out_rows, int64_t out_cols, int64_t ldo, hipStream_t st) {
   const dim3 grid((unsigned)cdiv(out_cols, 64), (unsigned)cdiv(out_rows, 64));
+  TimedLaunch tl("weight_transpose", st);
   hipLaunchKernelGGL(transpose_pad_kernel, grid, dim3(256), 0, st, in, rows, cols, ldi, out, out_rows, out_cols,
                      ldo);
   return hipGetLastError();
@@ -84,6 +85,7 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(float* __restrict__ p, i
 
 hipError_t fill_zero(float* p, int64_t n, hipStream_t st) {
   if (n == 0) return hipSuccess;
+  TimedLaunch tl("fill_zero", st);
   hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, p, n);
   return hipGetLastError();
 }
@@ -99,7 +101,7 @@ template <int AMODE>
 using CfgTT = GemmCfg<256, 256, 2, 2, AMODE, OP_T, EPI_F32, false>;
 
 template <class Cfg>
-hipError_t launch(GemmArgs g, int splits, hipStream_t st) {
+hipError_t launch(const char* tag, GemmArgs g, int splits, hipStream_t st) {
   g.tiles_m = (int)cdiv(g.M, Cfg::BM);
   g.tiles_n = (int)cdiv(g.N, Cfg::BN);
   if (splits <= 1) {
@@ -107,18 +109,19 @@ hipError_t launch(GemmArgs g, int splits, hipStream_t st) {
     g.k_split = cdiv(g.K, Cfg::BK) * Cfg::BK;
   }
   const dim3 grid((unsigned)(g.tiles_m * g.tiles_n), (unsigned)splits);
+  TimedLaunch tl(tag, st);
   hipLaunchKernelGGL(gemm_kernel<Cfg>, grid, dim3(256), 0, st, g);
   return hipGetLastError();
 }
 
 // Dense product C[M x N] = A[M x K] * Bt[N x K]^T in bf16.
-hipError_t gemm_nt_bf16(const uint16_t* A, int64_t lda, const uint16_t* Bt, int64_t ldb, uint16_t* C, int64_t ldc,
+hipError_t gemm_nt_bf16(const char* tag, const uint16_t* A, int64_t lda, const uint16_t* Bt, int64_t ldb, uint16_t* C, int64_t ldc,
                         int64_t M, int64_t N, int64_t K, hipStream_t st) {
   GemmArgs g{};
   g.A = A; g.lda = lda; g.B = Bt; g.ldb = ldb; g.C = C; g.ldc = ldc;
   g.M = M; g.N = N; g.K = K; g.m_valid = M; g.ka_valid = K; g.kb_valid = K;
-  if (N <= 128) return launch<CfgNT<128, EPI_BF16, false>>(g, 1, st);
-  return launch<CfgNT<256, EPI_BF16, false>>(g, 1, st);
+  if (N <= 128) return launch<CfgNT<128, EPI_BF16, false>>(tag, g, 1, st);
+  return launch<CfgNT<256, EPI_BF16, false>>(tag, g, 1, st);
 }
 
 // Split plan of a K = T product: enough workgroups to cover the 256 CUs once,
@@ -128,6 +131,7 @@ struct SplitPlan {
   int64_t k_split;
 };
 SplitPlan plan_splits(int64_t M, int64_t N, int64_t K) {
+  if (K <= 0) return {0, 0};
   const int64_t tiles = cdiv(M, 256) * cdiv(N, 256);
   const int64_t steps = cdiv(K, 64);
   int64_t s = 256 / tiles;
@@ -145,7 +149,7 @@ size_t partial_bytes(int64_t M, int64_t N, int64_t K) {
 // keeping rows m < rows_out.  A is [K x M] dense (OP_T) or 2:4 compressed
 // along M (OP_TSP); B is [K x N] dense.
 template <int AMODE>
-hipError_t gemm_tt_f32(const uint16_t* A, int64_t lda, const uint8_t* Am, int64_t ldam, const uint16_t* B,
+hipError_t gemm_tt_f32(const char* tag, const uint16_t* A, int64_t lda, const uint8_t* Am, int64_t ldam, const uint16_t* B,
                        int64_t ldb, int64_t M, int64_t N, int64_t K, float* part, float* out, int64_t rows_out,
                        bool transpose, int64_t ldo, hipStream_t st) {
   if (K == 0) return hipSuccess;
@@ -154,9 +158,10 @@ hipError_t gemm_tt_f32(const uint16_t* A, int64_t lda, const uint8_t* Am, int64_
   g.A = A; g.lda = lda; g.Am = Am; g.ldam = ldam; g.B = B; g.ldb = ldb;
   g.M = M; g.N = N; g.K = K; g.m_valid = M; g.ka_valid = K; g.kb_valid = K;
   g.k_split = p.k_split; g.C = part; g.ldc = N;
-  hipError_t e = launch<CfgTT<AMODE>>(g, p.splits, st);
+  hipError_t e = launch<CfgTT<AMODE>>(tag, g, p.splits, st);
   if (e != hipSuccess) return e;
   const int64_t n_out = rows_out * N;
+  TimedLaunch tl("splitk_reduce", st);
   hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)cdiv(n_out, 256)), dim3(256), 0, st, part, p.splits,
                      M, N, rows_out, transpose ? 1 : 0, out, ldo);
   return hipGetLastError();
@@ -235,7 +240,7 @@ hipError_t run_spmm24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, 
   g.B = bt; g.ldb = ldb;
   g.M = M; g.N = N; g.K = pad64(K); g.m_valid = M; g.ka_valid = pad64(K); g.kb_valid = K;
   g.C = c; g.ldc = N;
-  return launch<CfgSP>(g, 1, st);
+  return launch<CfgSP>("spmm24", g, 1, st);
 }
 
 hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
@@ -247,14 +252,14 @@ hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
   ELAS_TRY(transpose_pad(a.U_down, F, r, r, w.U_downT, r, Fp, Fp, st));    // [r x Fp], zero cols >= F
   ELAS_TRY(transpose_pad(a.V_down, r, d, d, w.V_downT, d, r, r, st));      // [d x r]
   // P = x U_up
-  ELAS_TRY(gemm_nt_bf16(a.x, d, w.U_upT, d, a.P, r, T, r, d, st));
+  ELAS_TRY(gemm_nt_bf16("k1_up_gemm", a.x, d, w.U_upT, d, a.P, r, T, r, d, st));
   // H^T = V_up^T P^T with ReLU^2 + 2:4 selection + compression in the epilogue
   {
     GemmArgs g{};
     g.A = w.V_upT; g.lda = r; g.B = a.P; g.ldb = r;
     g.M = Fp; g.N = T; g.K = r; g.m_valid = Fp; g.ka_valid = r; g.kb_valid = r;
     g.sv = a.s_vals; g.sm = a.s_meta; g.ldv = vals_ld(F); g.ldm = meta_ld(F);
-    ELAS_TRY(launch<CfgNT<256, EPI_SPARSIFY, true>>(g, 1, st));
+    ELAS_TRY(launch<CfgNT<256, EPI_SPARSIFY, true>>("k2_up_relu2_sparsify", g, 1, st));
   }
   // Z = S U_down on the 2:4 operand
   {
@@ -263,10 +268,10 @@ hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
     g.B = w.U_downT; g.ldb = Fp;
     g.M = T; g.N = r; g.K = Fp; g.m_valid = T; g.ka_valid = Fp; g.kb_valid = Fp;
     g.C = a.Z; g.ldc = r;
-    ELAS_TRY(launch<CfgSP>(g, 1, st));
+    ELAS_TRY(launch<CfgSP>("k3_spmm_down", g, 1, st));
   }
   // Y = Z V_down
-  ELAS_TRY(gemm_nt_bf16(a.Z, r, w.V_downT, r, a.y, d, T, d, r, st));
+  ELAS_TRY(gemm_nt_bf16("k4_down_gemm", a.Z, r, w.V_downT, r, a.y, d, T, d, r, st));
   return hipSuccess;
 }
 
@@ -282,19 +287,19 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
   }
   const BwdWs w = bwd_ws((char*)a.ws, T, d, F, r);
   // dZ = dY V_down^T   (V_down [r x d] is already the K-contiguous operand)
-  ELAS_TRY(gemm_nt_bf16(a.dy, d, a.V_down, d, w.dZ, r, T, r, d, st));
+  ELAS_TRY(gemm_nt_bf16("b1_dZ", a.dy, d, a.V_down, d, w.dZ, r, T, r, d, st));
   // dV_down = Z^T dY
-  ELAS_TRY(gemm_tt_f32<OP_T>(a.Z, r, nullptr, 0, a.dy, d, r, d, T, w.part, a.dV_down, r, false, d, st));
+  ELAS_TRY(gemm_tt_f32<OP_T>("b2_dV_down", a.Z, r, nullptr, 0, a.dy, d, r, d, T, w.part, a.dV_down, r, false, d, st));
   // dH = (dZ U_down^T) * mask * 2 relu(H), computed as dS^T = U_down dZ^T
   {
     GemmArgs g{};
     g.A = a.U_down; g.lda = r; g.B = w.dZ; g.ldb = r;
     g.M = Fp; g.N = T; g.K = r; g.m_valid = F; g.ka_valid = r; g.kb_valid = r;
     g.sv = a.s_vals; g.sm = a.s_meta; g.ldv = ldv; g.ldm = ldm; g.dv = w.dH;
-    ELAS_TRY(launch<CfgNT<256, EPI_DH, true>>(g, 1, st));
+    ELAS_TRY(launch<CfgNT<256, EPI_DH, true>>("b3_dH_masked", g, 1, st));
   }
   // dU_down = S^T dZ from the compressed S
-  ELAS_TRY(gemm_tt_f32<OP_TSP>(a.s_vals, ldv, a.s_meta, ldm, w.dZ, r, Fp, r, T, w.part, a.dU_down, F, false, r,
+  ELAS_TRY(gemm_tt_f32<OP_TSP>("b4_dU_down", a.s_vals, ldv, a.s_meta, ldm, w.dZ, r, Fp, r, T, w.part, a.dU_down, F, false, r,
                                st));
   // dP = dH V_up^T on the 2:4 operand (V_up [r x F] is already K-contiguous)
   {
@@ -303,14 +308,14 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
     g.B = a.V_up; g.ldb = F;
     g.M = T; g.N = r; g.K = Fp; g.m_valid = T; g.ka_valid = Fp; g.kb_valid = F;
     g.C = w.dP; g.ldc = r;
-    ELAS_TRY(launch<CfgSP>(g, 1, st));
+    ELAS_TRY(launch<CfgSP>("b5_spmm_dP", g, 1, st));
   }
   // dV_up = P^T dH, computed as dV_up^T = dH^T P and written transposed
-  ELAS_TRY(gemm_tt_f32<OP_TSP>(w.dH, ldv, a.s_meta, ldm, a.P_in, r, Fp, r, T, w.part, a.dV_up, F, true, F, st));
+  ELAS_TRY(gemm_tt_f32<OP_TSP>("b6_dV_up", w.dH, ldv, a.s_meta, ldm, a.P_in, r, Fp, r, T, w.part, a.dV_up, F, true, F, st));
   // dU_up = x^T dP
-  ELAS_TRY(gemm_tt_f32<OP_T>(a.x, d, nullptr, 0, w.dP, r, d, r, T, w.part, a.dU_up, d, false, r, st));
+  ELAS_TRY(gemm_tt_f32<OP_T>("b7_dU_up", a.x, d, nullptr, 0, w.dP, r, d, r, T, w.part, a.dU_up, d, false, r, st));
   // dx = dP U_up^T   (U_up [d x r] is already K-contiguous)
-  ELAS_TRY(gemm_nt_bf16(w.dP, r, a.U_up, r, a.dx, d, T, d, r, st));
+  ELAS_TRY(gemm_nt_bf16("b8_dx", w.dP, r, a.U_up, r, a.dx, d, T, d, r, st));
   return hipSuccess;
 }
 

@@ -6,9 +6,9 @@
 // BM x BN tile of C.  The contraction runs in steps of BK (64 dense, or 128
 // dense = 64 kept values for the 2:4 operand).  Both operands are staged in
 // LDS in "K-contiguous rows": row r of a tile holds BK (or 128) contraction
-// elements as 16-byte chunks; chunk c of row r lives at chunk position
-// c ^ (r & 7), so the eight lanes that read one 16-byte chunk each from eight
-// consecutive rows hit eight different bank groups.  LDS is double-buffered;
+// elements as 16-byte chunks, XOR-swizzled (see swz) so that reads and writes
+// of one chunk position across 8 rows hit 8 different bank groups.  LDS is
+// double-buffered;
 // the next step's global loads are issued into registers before the current
 // step's MFMAs and written to the other LDS buffer after them, so there is one
 // barrier per step.
@@ -87,7 +87,11 @@ struct GemmCfg {
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be a multiple of 32");
 };
 
-__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ (row & 7); }
+// LDS chunk swizzle.  Fragment reads touch 8 consecutive rows at one chunk;
+// the transposing stagers write rows 8 apart (rb*8 + j) at one chunk.  XOR-ing
+// the chunk with (row ^ row/8) & 7 spreads both patterns over 8 different
+// 16-byte bank groups.
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row ^ (row >> 3)) & 7); }
 
 // ---- transposes of 8x8 bf16 blocks held as 8 rows of uint4 ----------------
 // in[i] holds row i (8 consecutive elements); out[j] receives column j (the 8
@@ -179,9 +183,10 @@ struct Stager {
             if constexpr (MODE == OP_T) {
               v = *(const uint4*)(p + gk * ld + grow);
             } else {
+              // raw kept values + codes; expanded in store(), after the MFMAs,
+              // so the loads stay in flight during the current step
               const uint2 kept = *(const uint2*)(p + gk * ld + grow / 2);
-              const uint32_t codes = pm[gk * ldm + grow / 8];
-              v = expand2(kept, codes);
+              v = make_uint4(kept.x, kept.y, pm[gk * ldm + grow / 8], 0u);
             }
           }
           r[8 * b + i] = v;
@@ -205,7 +210,12 @@ struct Stager {
         const int rb = u % (ROWS / 8), kb = u / (ROWS / 8);
         uint4 in[8], out[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) in[i] = r[8 * b + i];
+        for (int i = 0; i < 8; ++i) {
+          if constexpr (MODE == OP_TSP)
+            in[i] = expand2(make_uint2(r[8 * b + i].x, r[8 * b + i].y), r[8 * b + i].z);
+          else
+            in[i] = r[8 * b + i];
+        }
         transpose8x8(in, out);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {

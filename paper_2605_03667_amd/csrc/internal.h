@@ -13,6 +13,21 @@ inline int64_t vals_ld(int64_t n) { return 32 * ((n + 63) / 64); }
 inline int64_t meta_ld(int64_t n) { return 8 * ((n + 63) / 64); }
 inline int64_t pad64(int64_t n) { return 64 * ((n + 63) / 64); }
 
+// timing.hip: brackets one launch with events when timing is enabled
+bool timing_enabled();
+class TimedLaunch {
+ public:
+  TimedLaunch(const char* tag, hipStream_t stream);
+  ~TimedLaunch();
+  TimedLaunch(const TimedLaunch&) = delete;
+  TimedLaunch& operator=(const TimedLaunch&) = delete;
+
+ private:
+  const char* tag_;
+  hipStream_t stream_;
+  hipEvent_t start_ = nullptr, stop_ = nullptr;
+};
+
 // sparsify.hip
 hipError_t launch_sparsify24(const uint16_t* h, int64_t M, int64_t N, bool raw,
                              uint16_t* vals, uint8_t* meta, hipStream_t stream);

@@ -58,6 +58,7 @@ hipError_t launch_sparsify24(const uint16_t* h, int64_t M, int64_t N, bool raw, 
   const int64_t chunks = ldv / 8;             // 16 features per thread, padding included
   const int64_t threads = M * chunks;
   const dim3 grid((unsigned)((threads + 255) / 256)), block(256);
+  TimedLaunch tl("sparsify24", stream);
   if (raw)
     hipLaunchKernelGGL(sparsify24_kernel<true>, grid, block, 0, stream, h, M, N, chunks, vals, meta, ldv, ldm);
   else
