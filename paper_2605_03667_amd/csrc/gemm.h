@@ -2,16 +2,22 @@
 // accumulation, one template covering every product of the ELAS low-rank FFN
 // (forward and backward).
 //
-// Tiling: a workgroup of 256 threads (4 wave64s, WAVES_M x WAVES_N) owns a
-// BM x BN tile of C.  The contraction runs in steps of BK (64 dense, or 128
-// dense = 64 kept values for the 2:4 operand).  Both operands are staged in
-// LDS in "K-contiguous rows": row r of a tile holds BK (or 128) contraction
-// elements as 16-byte chunks, XOR-swizzled (see swz) so that reads and writes
-// of one chunk position across 8 rows hit 8 different bank groups.  LDS is
-// double-buffered;
-// the next step's global loads are issued into registers before the current
-// step's MFMAs and written to the other LDS buffer after them, so there is one
-// barrier per step.
+// Tiling: a workgroup of WAVES_M x WAVES_N wave64s owns a BM x BN tile of C.
+// The contraction runs in steps of BK (64 dense, or 128 dense = 64 kept
+// values for the 2:4 operand).  Both operands are staged in LDS in
+// "K-contiguous rows": row r of a tile holds BK (or 128) contraction elements
+// as 16-byte chunks, XOR-swizzled (see swz) so that reads and writes of one
+// chunk position across 8 rows hit 8 different bank groups.
+//
+// Staging.  When both operands are K-contiguous in memory (OP_K / OP_SP) the
+// tiles go straight from global memory to LDS with global_load_lds_dwordx4
+// (no registers on the way), through STAGES LDS buffers: the loads of step
+// s + STAGES - 1 are issued while step s computes, and each wave waits only
+// for its own loads of step s (an exact vmcnt) before a plain s_barrier.
+// Lanes whose chunk lies outside the matrix load from a zero block.
+// Otherwise (a transposed operand) the next step's loads go to registers
+// before the current step's MFMAs and are written, transposed, to the other
+// of two LDS buffers after them.  Either way there is one barrier per step.
 //
 // Operand modes:
 //   OP_K    operand stored [rows x K] row-major (K contiguous): 16-byte copies.
@@ -68,12 +74,16 @@ struct GemmArgs {
   int tiles_m, tiles_n;
 };
 
-template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int AMODE_, int BMODE_, int EPI_, bool M_FAST_>
+template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int AMODE_, int BMODE_, int EPI_, bool M_FAST_,
+          int STAGES_ = 2>
 struct GemmCfg {
   static constexpr int BM = BM_, BN = BN_, WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
+  static constexpr int NW = WAVES_M_ * WAVES_N_, NT = 64 * NW;
   static constexpr int AMODE = AMODE_, BMODE = BMODE_, EPI = EPI_;
   static constexpr bool M_FAST = M_FAST_;   // consecutive tiles walk M (true) or N (false)
   static constexpr bool SPARSE = AMODE_ == OP_SP;
+  static constexpr bool DIRECT = (AMODE_ == OP_K || AMODE_ == OP_SP) && BMODE_ == OP_K;
+  static constexpr int STAGES = STAGES_;
   static constexpr int BK = SPARSE ? 128 : 64;         // dense contraction per step
   static constexpr int A_ROWB = 128;                     // bytes per LDS row of A (64 values)
   static constexpr int B_ROWB = SPARSE ? 256 : 128;      // bytes per LDS row of B
@@ -83,8 +93,11 @@ struct GemmCfg {
   static constexpr int STAGE = A_BYTES + AM_BYTES + B_BYTES;
   static constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
   static constexpr int FM = TM / 32, FN = TN / 32;
-  static_assert(WAVES_M * WAVES_N == 4, "4 waves");
+  static_assert(NW == 4 || NW == 8, "4 or 8 waves");
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be a multiple of 32");
+  static_assert(DIRECT || STAGES_ == 2, "register staging uses two LDS buffers");
+  static_assert(STAGES_ == 2 || STAGES_ == 3, "2 or 3 stages");
+  static_assert(STAGES_ * STAGE <= 160 * 1024, "LDS");
 };
 
 // LDS chunk swizzle.  Fragment reads touch 8 consecutive rows at one chunk;
@@ -130,129 +143,147 @@ __device__ __forceinline__ uint4 expand2(uint2 kept, uint32_t codes) {
   return make_uint4(d[0], d[1], d[2], d[3]);
 }
 
-// ---- operand staging --------------------------------------------------------
-// Registers that carry one K step of an operand from global memory to LDS.
-template <int ROWS, int ROWB, int MODE>
-struct Stager {
-  // OP_K / OP_SP: ROWS*ROWB/16 chunks of 16 bytes, CH per thread.
-  static constexpr int CHUNKS_PER_ROW = ROWB / 16;
-  static constexpr int CH = (MODE == OP_K || MODE == OP_SP) ? ROWS * CHUNKS_PER_ROW / 256 : 1;
-  // OP_T / OP_TSP: (BK/8) x (ROWS/8) blocks of 8x8, NB per thread (BK = 64).
-  static constexpr int NB = (MODE == OP_T || MODE == OP_TSP) ? (64 / 8) * (ROWS / 8) / 256 : 1;
-  static_assert(MODE == OP_T || MODE == OP_TSP || (ROWS * CHUNKS_PER_ROW) % 256 == 0, "chunks");
-  static_assert(!(MODE == OP_T || MODE == OP_TSP) || ((64 / 8) * (ROWS / 8)) % 256 == 0, "blocks");
-  uint4 r[(MODE == OP_T || MODE == OP_TSP) ? 8 * NB : CH];
+// ---- direct global -> LDS staging ------------------------------------------
+// Zeros read by lanes whose chunk lies outside the matrix.
+static __device__ __attribute__((aligned(16))) uint4 g_dma_zero[1];
 
-  // Global loads of the step starting at contraction index k0.
-  //   p, ld:      operand base and element pitch;
-  //   row0:       first tile row; rows_valid: rows that exist;
-  //   k_valid:    contraction entries that exist (dense count).
-  __device__ __forceinline__ void load(const uint16_t* __restrict__ p, int64_t ld, const uint8_t* __restrict__ pm,
-                                       int64_t ldm, int64_t row0, int64_t rows_valid, int64_t k0,
-                                       int64_t k_valid, int tid) {
-    if constexpr (MODE == OP_K || MODE == OP_SP) {
-      // OP_SP rows hold kept values: a 16-byte chunk is 8 values = 16 dense K.
-      constexpr int KPC = MODE == OP_SP ? 16 : 8;   // dense K per chunk
-#pragma unroll
-      for (int i = 0; i < CH; ++i) {
-        const int q = i * 256 + tid;
-        const int row = q / CHUNKS_PER_ROW, c = q % CHUNKS_PER_ROW;
-        const int64_t grow = row0 + row;
-        const int64_t gk = k0 + (int64_t)c * KPC;
-        uint4 v = make_uint4(0u, 0u, 0u, 0u);
-        if (grow < rows_valid && gk < k_valid) {
-          const uint16_t* src = p + grow * ld + (MODE == OP_SP ? gk / 2 : gk);
-          v = *(const uint4*)src;
-        }
-        r[i] = v;
-      }
-    } else {
-      // 8x8 blocks: block b -> (kb, rb) with rb fastest so a wave's lanes read
-      // consecutive 16-byte pieces of the same K-row.
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const int u = b * 256 + tid;
-        const int rb = u % (ROWS / 8), kb = u / (ROWS / 8);
-        const int64_t grow = row0 + rb * 8;
-        const bool rok = grow < rows_valid;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int64_t gk = k0 + kb * 8 + i;
-          uint4 v = make_uint4(0u, 0u, 0u, 0u);
-          if (rok && gk < k_valid) {
-            if constexpr (MODE == OP_T) {
-              v = *(const uint4*)(p + gk * ld + grow);
-            } else {
-              // raw kept values + codes; expanded in store(), after the MFMAs,
-              // so the loads stay in flight during the current step
-              const uint2 kept = *(const uint2*)(p + gk * ld + grow / 2);
-              v = make_uint4(kept.x, kept.y, pm[gk * ldm + grow / 8], 0u);
-            }
-          }
-          r[8 * b + i] = v;
-        }
-      }
-    }
-  }
+__device__ __forceinline__ uint32_t lds_u32(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+// One wave-wide LDS DMA: lane i's 16 (or 4) bytes land at LDS address
+// lds_wave_base + 16 i (4 i).  The base must be wave-uniform (it goes to M0).
+// Issued through inline asm so that the compiler does not guard every later
+// LDS access with a full vmcnt(0); the kernel waits with exact counts itself.
+__device__ __forceinline__ void dma_b128(const void* g, uint32_t lds_wave_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_wave_base) : "memory", "m0");
+}
+__device__ __forceinline__ void dma_b32(const void* g, uint32_t lds_wave_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds_wave_base) : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// Workgroup barrier without a memory fence (LDS DMA completion is covered by
+// the explicit vmcnt waits; the empty memory clobber keeps the compiler from
+// moving LDS reads across it).
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-  __device__ __forceinline__ void store(char* lds, int tid) const {
-    if constexpr (MODE == OP_K || MODE == OP_SP) {
+// A [ROWS x ROWB] K-contiguous tile (or the kept values of a 2:4 tile) copied
+// by DMA: the tile is cut into 1 KB blocks (8 or 4 rows), PER_WAVE blocks per
+// wave.  Lane i fills LDS chunk position i of its block; it fetches the
+// global chunk that the swizzle maps there.
+template <int ROWS, int ROWB, bool KEPT, int NW>
+struct DmaTile {
+  static constexpr int BLOCKS = ROWS * ROWB / 1024;
+  static constexpr int PER_WAVE = BLOCKS / NW;
+  static_assert(BLOCKS % NW == 0, "blocks per wave");
+  static constexpr int KPC = KEPT ? 16 : 8;    // dense K per 16-byte chunk
+  __device__ __forceinline__ static void issue(const uint16_t* __restrict__ p, int64_t ld, int64_t row0,
+                                               int64_t rows_valid, int64_t k0, int64_t k_valid, char* lds,
+                                               int wave, int lane) {
 #pragma unroll
-      for (int i = 0; i < CH; ++i) {
-        const int q = i * 256 + tid;
-        const int row = q / CHUNKS_PER_ROW, c = q % CHUNKS_PER_ROW;
-        *(uint4*)(lds + row * ROWB + swz(row, c) * 16) = r[i];
-      }
-    } else {
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const int u = b * 256 + tid;
-        const int rb = u % (ROWS / 8), kb = u / (ROWS / 8);
-        uint4 in[8], out[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          if constexpr (MODE == OP_TSP)
-            in[i] = expand2(make_uint2(r[8 * b + i].x, r[8 * b + i].y), r[8 * b + i].z);
-          else
-            in[i] = r[8 * b + i];
-        }
-        transpose8x8(in, out);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int row = rb * 8 + j;
-          *(uint4*)(lds + row * ROWB + swz(row, kb) * 16) = out[j];
-        }
-      }
+    for (int j = 0; j < PER_WAVE; ++j) {
+      const int blk = wave * PER_WAVE + j;
+      const int off = blk * 1024 + lane * 16;
+      const int row = off / ROWB, pos = (off % ROWB) / 16;
+      const int c = swz(row, pos);           // swz is an involution in the chunk index
+      const int64_t grow = row0 + row, gk = k0 + (int64_t)c * KPC;
+      const void* src = (grow < rows_valid && gk < k_valid) ? (const void*)(p + grow * ld + (KEPT ? gk / 2 : gk))
+                                                           : (const void*)g_dma_zero;
+      dma_b128(src, __builtin_amdgcn_readfirstlane(lds_u32(lds + blk * 1024)));
     }
   }
 };
 
-// Metadata rows of a 2:4 A tile: BM rows x 16 bytes (128 dense K).
-template <int BM>
-struct MetaStager {
-  static constexpr int CH = BM * 16 / 16 / 256 > 0 ? BM / 256 : 1;
-  uint4 r;
-  __device__ __forceinline__ void load(const uint8_t* __restrict__ pm, int64_t ldm, int64_t row0,
-                                       int64_t rows_valid, int64_t k0, int64_t k_valid, int tid) {
-    r = make_uint4(0u, 0u, 0u, 0u);
-    if (tid < BM) {
-      const int64_t grow = row0 + tid;
-      if (grow < rows_valid) {
-        const uint8_t* src = pm + grow * ldm + k0 / 8;
-        // 8 bytes cover 64 dense K; the row's metadata ends at k_valid / 8.
-        if (k0 + 64 <= k_valid) {
-          const uint2 lo = *(const uint2*)src;
-          r.x = lo.x; r.y = lo.y;
+// Metadata of a 2:4 tile: ROWS rows x 16 bytes (128 dense K), dword DMA
+// (256 bytes = 16 rows per wave instruction).
+template <int ROWS, int NW>
+struct DmaMeta {
+  static constexpr int BLOCKS = ROWS * 16 / 256;
+  static constexpr int PER_WAVE = BLOCKS / NW;
+  static_assert(BLOCKS % NW == 0, "meta blocks per wave");
+  __device__ __forceinline__ static void issue(const uint8_t* __restrict__ pm, int64_t ldm, int64_t row0,
+                                               int64_t rows_valid, int64_t k0, int64_t k_valid, char* lds,
+                                               int wave, int lane) {
+#pragma unroll
+    for (int j = 0; j < PER_WAVE; ++j) {
+      const int blk = wave * PER_WAVE + j;
+      const int off = blk * 256 + lane * 4;
+      const int row = off / 16, dw = (off % 16) / 4;     // dword dw covers dense K 32 dw .. 32 dw + 31
+      const int64_t grow = row0 + row;
+      const void* src = (grow < rows_valid && k0 + 32 * (dw + 1) <= k_valid)
+                            ? (const void*)(pm + grow * ldm + k0 / 8 + dw * 4)
+                            : (const void*)g_dma_zero;
+      dma_b32(src, __builtin_amdgcn_readfirstlane(lds_u32(lds + blk * 256)));
+    }
+  }
+};
+
+// ---- register staging of transposed operands --------------------------------
+// Registers that carry one K step (64) of a [K x ROWS] operand from global
+// memory to LDS: each thread owns NB 8x8 blocks (8 K-rows x 8 consecutive row
+// elements), transposed in registers on the way to K-contiguous LDS rows.
+template <int ROWS, int MODE, int NT>
+struct Stager {
+  static constexpr int ROWB = 128;
+  static constexpr int NB = (64 / 8) * (ROWS / 8) / NT;
+  static_assert(MODE == OP_T || MODE == OP_TSP, "transposed operands only");
+  static_assert(((64 / 8) * (ROWS / 8)) % NT == 0, "blocks per thread");
+  uint4 r[8 * NB];
+
+  // Global loads of the step starting at contraction index k0 (row0: first
+  // tile row; rows_valid: rows that exist; k_valid: contraction rows that exist).
+  __device__ __forceinline__ void load(const uint16_t* __restrict__ p, int64_t ld, const uint8_t* __restrict__ pm,
+                                       int64_t ldm, int64_t row0, int64_t rows_valid, int64_t k0,
+                                       int64_t k_valid, int tid) {
+    // block b -> (kb, rb) with rb fastest so a wave's lanes read consecutive
+    // 16-byte pieces of the same K-row
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int u = b * NT + tid;
+      const int rb = u % (ROWS / 8), kb = u / (ROWS / 8);
+      const int64_t grow = row0 + rb * 8;
+      const bool rok = grow < rows_valid;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int64_t gk = k0 + kb * 8 + i;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (rok && gk < k_valid) {
+          if constexpr (MODE == OP_T) {
+            v = *(const uint4*)(p + gk * ld + grow);
+          } else {
+            // raw kept values + codes; expanded in store(), after the MFMAs,
+            // so the loads stay in flight during the current step
+            const uint2 kept = *(const uint2*)(p + gk * ld + grow / 2);
+            v = make_uint4(kept.x, kept.y, pm[gk * ldm + grow / 8], 0u);
+          }
         }
-        if (k0 + 128 <= k_valid) {
-          const uint2 hi = *(const uint2*)(src + 8);
-          r.z = hi.x; r.w = hi.y;
-        }
+        r[8 * b + i] = v;
       }
     }
   }
+
   __device__ __forceinline__ void store(char* lds, int tid) const {
-    if (tid < BM) *(uint4*)(lds + tid * 16) = r;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int u = b * NT + tid;
+      const int rb = u % (ROWS / 8), kb = u / (ROWS / 8);
+      uint4 in[8], out[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        if constexpr (MODE == OP_TSP)
+          in[i] = expand2(make_uint2(r[8 * b + i].x, r[8 * b + i].y), r[8 * b + i].z);
+        else
+          in[i] = r[8 * b + i];
+      }
+      transpose8x8(in, out);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int row = rb * 8 + j;
+        *(uint4*)(lds + row * ROWB + swz(row, kb) * 16) = out[j];
+      }
+    }
   }
 };
 
@@ -267,11 +298,12 @@ __device__ __forceinline__ int xcd_remap(int pid, int total) {
 }
 
 template <class Cfg>
-__global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs g) {
-  constexpr int BM = Cfg::BM, BN = Cfg::BN, BK = Cfg::BK;
+__global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
+  constexpr int BM = Cfg::BM, BN = Cfg::BN, BK = Cfg::BK, NT = Cfg::NT, NW = Cfg::NW;
   constexpr int FM = Cfg::FM, FN = Cfg::FN, TM = Cfg::TM, TN = Cfg::TN;
   constexpr bool SPARSE = Cfg::SPARSE;
-  __shared__ __attribute__((aligned(16))) char smem[2 * Cfg::STAGE];
+  constexpr int STAGES = Cfg::STAGES;
+  __shared__ __attribute__((aligned(1024))) char smem[STAGES * Cfg::STAGE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -285,24 +317,6 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs g) {
   const int64_t kend = kbeg + g.k_split < g.K ? kbeg + g.k_split : g.K;
   const int nsteps = (int)((kend - kbeg + BK - 1) / BK);
 
-  using SA = Stager<BM, Cfg::A_ROWB, Cfg::AMODE>;
-  using SB = Stager<BN, Cfg::B_ROWB, Cfg::BMODE>;
-  SA sa;
-  SB sb;
-  MetaStager<BM> sm;
-
-  auto load_step = [&](int64_t k0) {
-    sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, k0, g.ka_valid, tid);
-    if constexpr (SPARSE) sm.load(g.Am, g.ldam, m0, g.m_valid, k0, g.ka_valid, tid);
-    sb.load(g.B, g.ldb, nullptr, 0, n0, g.N, k0, g.kb_valid, tid);
-  };
-  auto store_step = [&](int buf) {
-    char* base = smem + buf * Cfg::STAGE;
-    sa.store(base, tid);
-    if constexpr (SPARSE) sm.store(base + Cfg::A_BYTES, tid);
-    sb.store(base + Cfg::A_BYTES + Cfg::AM_BYTES, tid);
-  };
-
   f32x16 acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
@@ -313,15 +327,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs g) {
 
   const int lrow = lane & 31, lhalf = lane >> 5;
 
-  if (nsteps > 0) {
-    load_step(kbeg);
-    store_step(0);
-    __syncthreads();
-  }
-  for (int s = 0; s < nsteps; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < nsteps) load_step(kbeg + (int64_t)(s + 1) * BK);
-    const char* lA = smem + buf * Cfg::STAGE;
+  // MFMAs of one K step on the LDS stage at `base`.
+  auto compute = [&](const char* base) {
+    const char* lA = base;
     const char* lM = lA + Cfg::A_BYTES;
     const char* lB = lM + Cfg::AM_BYTES;
     if constexpr (!SPARSE) {
@@ -377,8 +385,62 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs g) {
             acc[i][j] = __builtin_amdgcn_smfmac_f32_32x32x32_bf16(af[i], bfr[j], acc[i][j], idx[i], 0, 0);
       }
     }
-    if (s + 1 < nsteps) store_step(buf ^ 1);
-    __syncthreads();
+  };
+
+  if constexpr (Cfg::DIRECT) {
+    using TA = DmaTile<BM, Cfg::A_ROWB, SPARSE, NW>;
+    using TB = DmaTile<BN, Cfg::B_ROWB, false, NW>;
+    using TMeta = DmaMeta<BM, (SPARSE ? NW : 1)>;
+    constexpr int LOADS = TA::PER_WAVE + TB::PER_WAVE + (SPARSE ? TMeta::PER_WAVE : 0);   // per wave per step
+    auto issue = [&](int step) {
+      const int64_t k0 = kbeg + (int64_t)step * BK;
+      char* base = smem + (step % STAGES) * Cfg::STAGE;
+      TA::issue(g.A, g.lda, m0, g.m_valid, k0, g.ka_valid, base, wave, lane);
+      if constexpr (SPARSE) TMeta::issue(g.Am, g.ldam, m0, g.m_valid, k0, g.ka_valid, base + Cfg::A_BYTES, wave, lane);
+      TB::issue(g.B, g.ldb, n0, g.N, k0, g.kb_valid, base + Cfg::A_BYTES + Cfg::AM_BYTES, wave, lane);
+    };
+#pragma unroll
+    for (int p = 0; p < STAGES - 1; ++p)
+      if (p < nsteps) issue(p);
+    for (int s = 0; s < nsteps; ++s) {
+      // wait for this wave's loads of step s: the loads of later steps already
+      // issued (at most STAGES - 2 steps) may stay in flight
+      if constexpr (STAGES == 3) {
+        if (s + 1 < nsteps)
+          wait_vmcnt<LOADS>();
+        else
+          wait_vmcnt<0>();
+      } else {
+        wait_vmcnt<0>();
+      }
+      lds_barrier();   // every wave's loads of step s landed; step s-1's reads are done
+      if (s + STAGES - 1 < nsteps) issue(s + STAGES - 1);
+      compute(smem + (s % STAGES) * Cfg::STAGE);
+    }
+  } else {
+    Stager<BM, Cfg::AMODE, NT> sa;
+    Stager<BN, Cfg::BMODE, NT> sb;
+    auto load_step = [&](int64_t k0) {
+      sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, k0, g.ka_valid, tid);
+      sb.load(g.B, g.ldb, nullptr, 0, n0, g.N, k0, g.kb_valid, tid);
+    };
+    auto store_step = [&](int buf) {
+      char* base = smem + buf * Cfg::STAGE;
+      sa.store(base, tid);
+      sb.store(base + Cfg::A_BYTES, tid);
+    };
+    if (nsteps > 0) {
+      load_step(kbeg);
+      store_step(0);
+      __syncthreads();
+    }
+    for (int s = 0; s < nsteps; ++s) {
+      const int buf = s & 1;
+      if (s + 1 < nsteps) load_step(kbeg + (int64_t)(s + 1) * BK);
+      compute(smem + buf * Cfg::STAGE);
+      if (s + 1 < nsteps) store_step(buf ^ 1);
+      __syncthreads();
+    }
   }
 
   // ---------------------------------------------------------------- epilogues
