@@ -45,6 +45,8 @@
 //     16h; B lane half c then takes memory K [8c, 8c+8) and [16+8c, 16+8c+8).
 #pragma once
 
+#include <type_traits>
+
 #include "device.h"
 
 namespace elas {
@@ -75,8 +77,11 @@ struct GemmArgs {
 };
 
 template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int AMODE_, int BMODE_, int EPI_, bool M_FAST_,
-          int STAGES_ = 2>
+          int STAGES_ = 2, bool SPREAD_ = false>
 struct GemmCfg {
+  // SPREAD: issue the next stage's loads in four parts between the MFMA
+  // sub-steps instead of all at the start of a step.
+  static constexpr bool SPREAD = SPREAD_;
   static constexpr int BM = BM_, BN = BN_, WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
   static constexpr int NW = WAVES_M_ * WAVES_N_, NT = 64 * NW;
   static constexpr int AMODE = AMODE_, BMODE = BMODE_, EPI = EPI_;
@@ -179,11 +184,14 @@ struct DmaTile {
   static constexpr int PER_WAVE = BLOCKS / NW;
   static_assert(BLOCKS % NW == 0, "blocks per wave");
   static constexpr int KPC = KEPT ? 16 : 8;    // dense K per 16-byte chunk
+  // Issue this wave's loads j in [J0, J1) for the step at k0 into the LDS
+  // buffer at byte address lds (wave-uniform).
+  template <int J0, int J1>
   __device__ __forceinline__ static void issue(const uint16_t* __restrict__ p, int64_t ld, int64_t row0,
-                                               int64_t rows_valid, int64_t k0, int64_t k_valid, char* lds,
+                                               int64_t rows_valid, int64_t k0, int64_t k_valid, uint32_t lds,
                                                int wave, int lane) {
 #pragma unroll
-    for (int j = 0; j < PER_WAVE; ++j) {
+    for (int j = J0; j < J1; ++j) {
       const int blk = wave * PER_WAVE + j;
       const int off = blk * 1024 + lane * 16;
       const int row = off / ROWB, pos = (off % ROWB) / 16;
@@ -191,7 +199,7 @@ struct DmaTile {
       const int64_t grow = row0 + row, gk = k0 + (int64_t)c * KPC;
       const void* src = (grow < rows_valid && gk < k_valid) ? (const void*)(p + grow * ld + (KEPT ? gk / 2 : gk))
                                                            : (const void*)g_dma_zero;
-      dma_b128(src, __builtin_amdgcn_readfirstlane(lds_u32(lds + blk * 1024)));
+      dma_b128(src, __builtin_amdgcn_readfirstlane(lds + blk * 1024));
     }
   }
 };
@@ -203,11 +211,12 @@ struct DmaMeta {
   static constexpr int BLOCKS = ROWS * 16 / 256;
   static constexpr int PER_WAVE = BLOCKS / NW;
   static_assert(BLOCKS % NW == 0, "meta blocks per wave");
+  template <int J0, int J1>
   __device__ __forceinline__ static void issue(const uint8_t* __restrict__ pm, int64_t ldm, int64_t row0,
-                                               int64_t rows_valid, int64_t k0, int64_t k_valid, char* lds,
+                                               int64_t rows_valid, int64_t k0, int64_t k_valid, uint32_t lds,
                                                int wave, int lane) {
 #pragma unroll
-    for (int j = 0; j < PER_WAVE; ++j) {
+    for (int j = J0; j < J1; ++j) {
       const int blk = wave * PER_WAVE + j;
       const int off = blk * 256 + lane * 4;
       const int row = off / 16, dw = (off % 16) / 4;     // dword dw covers dense K 32 dw .. 32 dw + 31
@@ -215,22 +224,25 @@ struct DmaMeta {
       const void* src = (grow < rows_valid && k0 + 32 * (dw + 1) <= k_valid)
                             ? (const void*)(pm + grow * ldm + k0 / 8 + dw * 4)
                             : (const void*)g_dma_zero;
-      dma_b32(src, __builtin_amdgcn_readfirstlane(lds_u32(lds + blk * 256)));
+      dma_b32(src, __builtin_amdgcn_readfirstlane(lds + blk * 256));
     }
   }
 };
 
 // ---- register staging of transposed operands --------------------------------
 // Registers that carry one K step (64) of a [K x ROWS] operand from global
-// memory to LDS: each thread owns NB 8x8 blocks (8 K-rows x 8 consecutive row
-// elements), transposed in registers on the way to K-contiguous LDS rows.
+// memory to LDS: each thread owns blocks of KR K-rows x 8 consecutive row
+// elements (KR = 8 for 256 threads, 4 for 512), transposed in registers on
+// the way to K-contiguous LDS rows (a block of 8 K-rows fills one 16-byte
+// chunk, a block of 4 K-rows one half chunk).
 template <int ROWS, int MODE, int NT>
 struct Stager {
   static constexpr int ROWB = 128;
-  static constexpr int NB = (64 / 8) * (ROWS / 8) / NT;
+  static constexpr int KR = NT >= 512 ? 4 : 8;
+  static constexpr int NB = (64 / KR) * (ROWS / 8) / NT;
   static_assert(MODE == OP_T || MODE == OP_TSP, "transposed operands only");
-  static_assert(((64 / 8) * (ROWS / 8)) % NT == 0, "blocks per thread");
-  uint4 r[8 * NB];
+  static_assert(((64 / KR) * (ROWS / 8)) % NT == 0 && NB >= 1, "blocks per thread");
+  uint4 r[KR * NB];
 
   // Global loads of the step starting at contraction index k0 (row0: first
   // tile row; rows_valid: rows that exist; k_valid: contraction rows that exist).
@@ -238,7 +250,7 @@ struct Stager {
                                        int64_t ldm, int64_t row0, int64_t rows_valid, int64_t k0,
                                        int64_t k_valid, int tid) {
     // block b -> (kb, rb) with rb fastest so a wave's lanes read consecutive
-    // 16-byte pieces of the same K-row
+    // pieces of the same K-row
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       const int u = b * NT + tid;
@@ -246,8 +258,8 @@ struct Stager {
       const int64_t grow = row0 + rb * 8;
       const bool rok = grow < rows_valid;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int64_t gk = k0 + kb * 8 + i;
+      for (int i = 0; i < KR; ++i) {
+        const int64_t gk = k0 + kb * KR + i;
         uint4 v = make_uint4(0u, 0u, 0u, 0u);
         if (rok && gk < k_valid) {
           if constexpr (MODE == OP_T) {
@@ -259,7 +271,7 @@ struct Stager {
             v = make_uint4(kept.x, kept.y, pm[gk * ldm + grow / 8], 0u);
           }
         }
-        r[8 * b + i] = v;
+        r[KR * b + i] = v;
       }
     }
   }
@@ -269,19 +281,36 @@ struct Stager {
     for (int b = 0; b < NB; ++b) {
       const int u = b * NT + tid;
       const int rb = u % (ROWS / 8), kb = u / (ROWS / 8);
-      uint4 in[8], out[8];
+      uint4 in[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < KR; ++i) {
         if constexpr (MODE == OP_TSP)
-          in[i] = expand2(make_uint2(r[8 * b + i].x, r[8 * b + i].y), r[8 * b + i].z);
+          in[i] = expand2(make_uint2(r[KR * b + i].x, r[KR * b + i].y), r[KR * b + i].z);
         else
-          in[i] = r[8 * b + i];
+          in[i] = r[KR * b + i];
       }
-      transpose8x8(in, out);
+      if constexpr (KR == 8) {
+        uint4 out[8];
+        transpose8x8(in, out);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int row = rb * 8 + j;
-        *(uint4*)(lds + row * ROWB + swz(row, kb) * 16) = out[j];
+        for (int j = 0; j < 8; ++j) {
+          const int row = rb * 8 + j;
+          *(uint4*)(lds + row * ROWB + swz(row, kb) * 16) = out[j];
+        }
+      } else {
+        // 4 K-rows: element j of the 4 rows -> half chunk (kb & 1) of chunk kb/2
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          uint32_t w[2];
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            const uint32_t x = ((const uint32_t*)&in[2 * q])[j >> 1];
+            const uint32_t y = ((const uint32_t*)&in[2 * q + 1])[j >> 1];
+            w[q] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
+          }
+          const int row = rb * 8 + j;
+          *(uint2*)(lds + row * ROWB + swz(row, kb >> 1) * 16 + (kb & 1) * 8) = make_uint2(w[0], w[1]);
+        }
       }
     }
   }
@@ -327,30 +356,39 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
 
   const int lrow = lane & 31, lhalf = lane >> 5;
 
-  // MFMAs of one K step on the LDS stage at `base`.
-  auto compute = [&](const char* base) {
+  // MFMAs of one K step on the LDS stage at `base`.  Fragments of sub-step
+  // kk+1 are read while sub-step kk's MFMAs run; hook(kk) runs between the
+  // reads and the MFMAs of sub-step kk (it issues part of the next stage's
+  // loads in the direct path).
+  auto compute = [&](const char* base, auto&& hook) __attribute__((always_inline)) {
     const char* lA = base;
     const char* lM = lA + Cfg::A_BYTES;
     const char* lB = lM + Cfg::AM_BYTES;
     if constexpr (!SPARSE) {
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {       // four k16 MFMA steps per 64-wide K step
-        bf16x8 af[FM], bfr[FN];
+      bf16x8 af[2][FM], bfr[2][FN];
+      auto read = [&](int kk, int slot) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
           const int row = wm * TM + i * 32 + lrow;
-          af[i] = *(const bf16x8*)(lA + row * 128 + swz(row, 2 * kk + lhalf) * 16);
+          af[slot][i] = *(const bf16x8*)(lA + row * 128 + swz(row, 2 * kk + lhalf) * 16);
         }
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
           const int row = wn * TN + j * 32 + lrow;
-          bfr[j] = *(const bf16x8*)(lB + row * 128 + swz(row, 2 * kk + lhalf) * 16);
+          bfr[slot][j] = *(const bf16x8*)(lB + row * 128 + swz(row, 2 * kk + lhalf) * 16);
         }
+      };
+      read(0, 0);
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {       // four k16 MFMA steps per 64-wide K step
+        const int cur = kk & 1;
+        if (kk + 1 < 4) read(kk + 1, cur ^ 1);
+        hook(kk);
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
           for (int j = 0; j < FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
       }
     } else {
       uint4 meta[FM];
@@ -359,30 +397,39 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         const int row = wm * TM + i * 32 + lrow;
         meta[i] = *(const uint4*)(lM + row * 16);
       }
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {       // four 32-wide smfmac steps per 128-wide K step
-        bf16x8 af[FM];
-        bf16x16 bfr[FN];
-        int idx[FM];
+      bf16x8 af[2][FM];
+      bf16x16 bfr[2][FN];
+      auto read = [&](int kk, int slot) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
           const int row = wm * TM + i * 32 + lrow;
-          af[i] = *(const bf16x8*)(lA + row * 128 + swz(row, 2 * kk + lhalf) * 16);
-          const uint32_t w = kk == 0 ? meta[i].x : kk == 1 ? meta[i].y : kk == 2 ? meta[i].z : meta[i].w;
-          idx[i] = (int)(w >> (16 * lhalf));
+          af[slot][i] = *(const bf16x8*)(lA + row * 128 + swz(row, 2 * kk + lhalf) * 16);
         }
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
           const int row = wn * TN + j * 32 + lrow;
           const bf16x8 lo = *(const bf16x8*)(lB + row * 256 + swz(row, 4 * kk + lhalf) * 16);
           const bf16x8 hi = *(const bf16x8*)(lB + row * 256 + swz(row, 4 * kk + 2 + lhalf) * 16);
-          bfr[j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
+          bfr[slot][j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
+        }
+      };
+      read(0, 0);
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {       // four 32-wide smfmac steps per 128-wide K step
+        const int cur = kk & 1;
+        if (kk + 1 < 4) read(kk + 1, cur ^ 1);
+        hook(kk);
+        int idx[FM];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+          const uint32_t w = kk == 0 ? meta[i].x : kk == 1 ? meta[i].y : kk == 2 ? meta[i].z : meta[i].w;
+          idx[i] = (int)(w >> (16 * lhalf));
         }
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
           for (int j = 0; j < FN; ++j)
-            acc[i][j] = __builtin_amdgcn_smfmac_f32_32x32x32_bf16(af[i], bfr[j], acc[i][j], idx[i], 0, 0);
+            acc[i][j] = __builtin_amdgcn_smfmac_f32_32x32x32_bf16(af[cur][i], bfr[cur][j], acc[i][j], idx[i], 0, 0);
       }
     }
   };
@@ -391,17 +438,38 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     using TA = DmaTile<BM, Cfg::A_ROWB, SPARSE, NW>;
     using TB = DmaTile<BN, Cfg::B_ROWB, false, NW>;
     using TMeta = DmaMeta<BM, (SPARSE ? NW : 1)>;
-    constexpr int LOADS = TA::PER_WAVE + TB::PER_WAVE + (SPARSE ? TMeta::PER_WAVE : 0);   // per wave per step
-    auto issue = [&](int step) {
+    constexpr int LA = TA::PER_WAVE, LB = TB::PER_WAVE, LM = SPARSE ? TMeta::PER_WAVE : 0;
+    constexpr int LOADS = LA + LB + LM;   // DMA instructions per wave per step
+    const uint32_t smem_lds = lds_u32(smem);
+    // Issue the loads of `step`, part q of 4 (A first half, A second half +
+    // metadata, B first half, B second half).
+    auto issue_part = [&](int step, auto q) __attribute__((always_inline)) {
       const int64_t k0 = kbeg + (int64_t)step * BK;
-      char* base = smem + (step % STAGES) * Cfg::STAGE;
-      TA::issue(g.A, g.lda, m0, g.m_valid, k0, g.ka_valid, base, wave, lane);
-      if constexpr (SPARSE) TMeta::issue(g.Am, g.ldam, m0, g.m_valid, k0, g.ka_valid, base + Cfg::A_BYTES, wave, lane);
-      TB::issue(g.B, g.ldb, n0, g.N, k0, g.kb_valid, base + Cfg::A_BYTES + Cfg::AM_BYTES, wave, lane);
+      const uint32_t base = smem_lds + (uint32_t)((step % STAGES) * Cfg::STAGE);
+      constexpr int Q = decltype(q)::value;
+      if constexpr (Q == 0) {
+        TA::template issue<0, LA / 2>(g.A, g.lda, m0, g.m_valid, k0, g.ka_valid, base, wave, lane);
+      } else if constexpr (Q == 1) {
+        TA::template issue<LA / 2, LA>(g.A, g.lda, m0, g.m_valid, k0, g.ka_valid, base, wave, lane);
+        if constexpr (SPARSE)
+          TMeta::template issue<0, LM>(g.Am, g.ldam, m0, g.m_valid, k0, g.ka_valid, base + Cfg::A_BYTES, wave, lane);
+      } else if constexpr (Q == 2) {
+        TB::template issue<0, LB / 2>(g.B, g.ldb, n0, g.N, k0, g.kb_valid, base + Cfg::A_BYTES + Cfg::AM_BYTES,
+                                      wave, lane);
+      } else {
+        TB::template issue<LB / 2, LB>(g.B, g.ldb, n0, g.N, k0, g.kb_valid, base + Cfg::A_BYTES + Cfg::AM_BYTES,
+                                       wave, lane);
+      }
+    };
+    auto issue_all = [&](int step) __attribute__((always_inline)) {
+      issue_part(step, std::integral_constant<int, 0>{});
+      issue_part(step, std::integral_constant<int, 1>{});
+      issue_part(step, std::integral_constant<int, 2>{});
+      issue_part(step, std::integral_constant<int, 3>{});
     };
 #pragma unroll
     for (int p = 0; p < STAGES - 1; ++p)
-      if (p < nsteps) issue(p);
+      if (p < nsteps) issue_all(p);
     for (int s = 0; s < nsteps; ++s) {
       // wait for this wave's loads of step s: the loads of later steps already
       // issued (at most STAGES - 2 steps) may stay in flight
@@ -414,17 +482,30 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         wait_vmcnt<0>();
       }
       lds_barrier();   // every wave's loads of step s landed; step s-1's reads are done
-      if (s + STAGES - 1 < nsteps) issue(s + STAGES - 1);
-      compute(smem + (s % STAGES) * Cfg::STAGE);
+      const int nxt = s + STAGES - 1;
+      const bool more = nxt < nsteps;
+      if constexpr (!Cfg::SPREAD) {
+        if (more) issue_all(nxt);
+      }
+      compute(smem + (s % STAGES) * Cfg::STAGE, [&](int kk) __attribute__((always_inline)) {
+        if constexpr (Cfg::SPREAD) {
+          if (more) {
+            if (kk == 0) issue_part(nxt, std::integral_constant<int, 0>{});
+            if (kk == 1) issue_part(nxt, std::integral_constant<int, 1>{});
+            if (kk == 2) issue_part(nxt, std::integral_constant<int, 2>{});
+            if (kk == 3) issue_part(nxt, std::integral_constant<int, 3>{});
+          }
+        }
+      });
     }
   } else {
     Stager<BM, Cfg::AMODE, NT> sa;
     Stager<BN, Cfg::BMODE, NT> sb;
-    auto load_step = [&](int64_t k0) {
+    auto load_step = [&](int64_t k0) __attribute__((always_inline)) {
       sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, k0, g.ka_valid, tid);
       sb.load(g.B, g.ldb, nullptr, 0, n0, g.N, k0, g.kb_valid, tid);
     };
-    auto store_step = [&](int buf) {
+    auto store_step = [&](int buf) __attribute__((always_inline)) {
       char* base = smem + buf * Cfg::STAGE;
       sa.store(base, tid);
       sb.store(base + Cfg::A_BYTES, tid);
@@ -436,9 +517,20 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     }
     for (int s = 0; s < nsteps; ++s) {
       const int buf = s & 1;
-      if (s + 1 < nsteps) load_step(kbeg + (int64_t)(s + 1) * BK);
-      compute(smem + buf * Cfg::STAGE);
-      if (s + 1 < nsteps) store_step(buf ^ 1);
+      const bool more = s + 1 < nsteps;
+      if (more) load_step(kbeg + (int64_t)(s + 1) * BK);
+      if constexpr (Cfg::AMODE == OP_T) {
+        // the next step's transposing LDS writes go in before the last
+        // sub-step's MFMAs, so they overlap the matrix cores' work
+        compute(smem + buf * Cfg::STAGE, [&](int kk) __attribute__((always_inline)) {
+          if (kk == 3 && more) store_step(buf ^ 1);
+        });
+      } else {
+        // the 2:4 expansion needs more registers than are free during the
+        // MFMAs (spills), so it runs after them
+        compute(smem + buf * Cfg::STAGE, [](int) {});
+        if (more) store_step(buf ^ 1);
+      }
       __syncthreads();
     }
   }
@@ -469,12 +561,54 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     // lane are features 8b + 4h + 0..3 of a 32-row block: one whole group of
     // 4 (Algorithm 1).  Lanes l and l+32 hold the even and odd groups of the
     // same 8 features, i.e. the two nibbles of one metadata byte.
+    //
+    // The tile's compressed rows (one per token: BM/2 kept values and BM/8
+    // metadata bytes) are staged in LDS so that global memory sees whole
+    // 16-byte (values) and 8-byte (metadata) pieces of each token row.  LDS
+    // rows are padded by 4 bytes so that the 32 lanes of a wave, which touch
+    // 32 different token rows at one column, hit 32 different banks.
+    constexpr int VP = BM + 4;            // bytes per LDS row of kept values (BM/2 bf16 + pad)
+    constexpr int MP = BM / 8 + 4;        // bytes per LDS row of metadata
+    constexpr int META_OFF = (BN * VP + 15) / 16 * 16;
+    static_assert(META_OFF + BN * MP <= STAGES * Cfg::STAGE, "epilogue staging fits in LDS");
+    char* lv = smem;
+    char* lm = smem + META_OFF;
+    const int64_t t_end = g.N - n0;                      // valid tokens in this tile (may exceed BN)
+    const int64_t f_end = g.M - m0;                      // valid features (multiple of 64)
+    __syncthreads();                                     // main-loop LDS reads are finished
+
+    if constexpr (Cfg::EPI == EPI_DH) {
+      // stored S rows of this tile -> LDS
+      constexpr int VCH = BN * (BM / 16);               // 16-byte value chunks
+#pragma unroll
+      for (int it = 0; it < VCH / NT; ++it) {
+        const int q = it * NT + tid, row = q / (BM / 16), c = q % (BM / 16);
+        if (row < t_end && c * 16 < f_end) {
+          const uint4 v = *(const uint4*)(g.sv + (n0 + row) * g.ldv + m0 / 2 + c * 8);
+          uint32_t* d = (uint32_t*)(lv + row * VP + c * 16);
+          d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
+        }
+      }
+      constexpr int MCH = BN * (BM / 64);               // 8-byte metadata chunks
+#pragma unroll
+      for (int it = 0; it < (MCH + NT - 1) / NT; ++it) {
+        const int q = it * NT + tid, row = q / (BM / 64), c = q % (BM / 64);
+        if (q < MCH && row < t_end && c * 64 < f_end) {
+          const uint2 v = *(const uint2*)(g.sm + (n0 + row) * g.ldm + m0 / 8 + c * 8);
+          uint32_t* d = (uint32_t*)(lm + row * MP + c * 8);
+          d[0] = v.x; d[1] = v.y;
+        }
+      }
+      __syncthreads();
+    }
+
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
-        const int64_t t = n0 + wn * TN + j * 32 + lrow;
-        const int64_t f32 = m0 + wm * TM + i * 32;     // first feature of the 32-row block
+        const int tl = wn * TN + j * 32 + lrow;         // token within the tile
+        const int fl = wm * TM + i * 32;                // first feature of the 32-row block
+        const bool ok = tl < t_end && fl < f_end;
         uint32_t pair[4], codes = 0;
         if constexpr (Cfg::EPI == EPI_SPARSIFY) {
 #pragma unroll
@@ -491,65 +625,69 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             pair[b] = f32_to_bf16_rne(a * a) | (f32_to_bf16_rne(c * c) << 16);
             codes |= code << (4 * b);
           }
-        } else {
-          // EPI_DH: read the stored group (values + code) and scale dS at the
-          // kept positions by 2 relu(h), relu(h) = bf16(sqrt(s)) exactly.
-          uint32_t sv[4] = {0u, 0u, 0u, 0u};
-          uint32_t word = 0;
-          if (t < g.N && f32 < g.M) {
-            // this lane's groups: 8b + 4h -> group index (f32/4) + 2b + h
-            word = *(const uint32_t*)(g.sm + t * g.ldm + f32 / 8);
+          const uint32_t other_codes = __shfl_xor(codes, 32);
+          if (ok) {
 #pragma unroll
             for (int b = 0; b < 4; ++b)
-              sv[b] = *(const uint32_t*)(g.sv + t * g.ldv + (f32 / 4 + 2 * b + lhalf) * 2);
-          }
-#pragma unroll
-          for (int b = 0; b < 4; ++b) {
-            const uint32_t code = (word >> (8 * b + 4 * lhalf)) & 0xFu;
-            const uint32_t i0 = code & 3u, i1 = code >> 2;
-            float ds[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) ds[q] = acc[i][j][4 * b + q];
-            const float d0 = i0 == 0u ? ds[0] : i0 == 1u ? ds[1] : ds[2];
-            const float d1 = i1 == 1u ? ds[1] : i1 == 2u ? ds[2] : ds[3];
-            const float s0 = bf16_to_f32(sv[b] & 0xFFFFu), s1 = bf16_to_f32(sv[b] >> 16);
-            const float r0 = (float)(__bf16)__builtin_sqrtf(s0);
-            const float r1 = (float)(__bf16)__builtin_sqrtf(s1);
-            const uint32_t o0 = __builtin_bit_cast(uint16_t, (__bf16)(d0 * 2.0f * r0));
-            const uint32_t o1 = __builtin_bit_cast(uint16_t, (__bf16)(d1 * 2.0f * r1));
-            pair[b] = o0 | (o1 << 16);
-            codes |= code << (4 * b);
-          }
-        }
-        // Lane pair (l, l+32) -> one 32-bit metadata word and 16 kept values
-        // (groups f32/4 .. f32/4+7).  Lane half 0 writes groups 0..3, half 1
-        // groups 4..7, 16 bytes each.
-        const uint32_t other_codes = __shfl_xor(codes, 32);
-        uint32_t give0 = lhalf ? pair[0] : pair[2];
-        uint32_t give1 = lhalf ? pair[1] : pair[3];
-        const uint32_t got0 = __shfl_xor(give0, 32);
-        const uint32_t got1 = __shfl_xor(give1, 32);
-        if (t < g.N && f32 < g.M) {
-          // groups in order: half 0 owns even groups (b -> 2b), half 1 odd (2b+1)
-          uint4 out;
-          if (lhalf == 0) {   // groups 0,1,2,3 = mine b0, other b0, mine b1, other b1
-            out = make_uint4(pair[0], got0, pair[1], got1);
-          } else {            // groups 4,5,6,7 = other b2, mine b2, other b3, mine b3
-            out = make_uint4(got0, pair[2], got1, pair[3]);
-          }
-          uint16_t* dst = (Cfg::EPI == EPI_SPARSIFY ? g.sv : g.dv) + t * g.ldv + f32 / 2 + lhalf * 8;
-          *(uint4*)dst = out;
-          if constexpr (Cfg::EPI == EPI_SPARSIFY) {
+              *(uint32_t*)(lv + tl * VP + (fl / 4 + 2 * b + lhalf) * 4) = pair[b];
             if (lhalf == 0) {
               uint32_t word = 0;
 #pragma unroll
               for (int b = 0; b < 4; ++b)
                 word |= (((codes >> (4 * b)) & 0xFu) | (((other_codes >> (4 * b)) & 0xFu) << 4)) << (8 * b);
-              *(uint32_t*)(g.sm + t * g.ldm + f32 / 8) = word;
+              *(uint32_t*)(lm + tl * MP + fl / 8) = word;
+            }
+          }
+        } else {
+          // EPI_DH: scale dS at the kept positions of the stored group by
+          // 2 relu(h), relu(h) = bf16(sqrt(s)) exactly; result in place.
+          if (ok) {
+            const uint32_t word = *(const uint32_t*)(lm + tl * MP + fl / 8);
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+              uint32_t* loc = (uint32_t*)(lv + tl * VP + (fl / 4 + 2 * b + lhalf) * 4);
+              const uint32_t sv = *loc;
+              const uint32_t code = (word >> (8 * b + 4 * lhalf)) & 0xFu;
+              const uint32_t i0 = code & 3u, i1 = code >> 2;
+              float ds[4];
+#pragma unroll
+              for (int q = 0; q < 4; ++q) ds[q] = acc[i][j][4 * b + q];
+              const float d0 = i0 == 0u ? ds[0] : i0 == 1u ? ds[1] : ds[2];
+              const float d1 = i1 == 1u ? ds[1] : i1 == 2u ? ds[2] : ds[3];
+              const float s0 = bf16_to_f32(sv & 0xFFFFu), s1 = bf16_to_f32(sv >> 16);
+              const float r0 = (float)(__bf16)__builtin_sqrtf(s0);
+              const float r1 = (float)(__bf16)__builtin_sqrtf(s1);
+              const uint32_t o0 = __builtin_bit_cast(uint16_t, (__bf16)(d0 * 2.0f * r0));
+              const uint32_t o1 = __builtin_bit_cast(uint16_t, (__bf16)(d1 * 2.0f * r1));
+              *loc = o0 | (o1 << 16);
             }
           }
         }
       }
+    __syncthreads();
+
+    // LDS -> global: whole 16-byte pieces of each token row
+    uint16_t* dst = Cfg::EPI == EPI_SPARSIFY ? g.sv : g.dv;
+    constexpr int VCH = BN * (BM / 16);
+#pragma unroll
+    for (int it = 0; it < VCH / NT; ++it) {
+      const int q = it * NT + tid, row = q / (BM / 16), c = q % (BM / 16);
+      if (row < t_end && c * 16 < f_end) {
+        const uint32_t* sp = (const uint32_t*)(lv + row * VP + c * 16);
+        *(uint4*)(dst + (n0 + row) * g.ldv + m0 / 2 + c * 8) = make_uint4(sp[0], sp[1], sp[2], sp[3]);
+      }
+    }
+    if constexpr (Cfg::EPI == EPI_SPARSIFY) {
+      constexpr int MCH = BN * (BM / 64);
+#pragma unroll
+      for (int it = 0; it < (MCH + NT - 1) / NT; ++it) {
+        const int q = it * NT + tid, row = q / (BM / 64), c = q % (BM / 64);
+        if (q < MCH && row < t_end && c * 64 < f_end) {
+          const uint32_t* sp = (const uint32_t*)(lm + row * MP + c * 8);
+          *(uint2*)(g.sm + (n0 + row) * g.ldm + m0 / 8 + c * 8) = make_uint2(sp[0], sp[1]);
+        }
+      }
+    }
   }
 }
 
