@@ -61,6 +61,41 @@ def executed_flops(tag: str, T: int, d: int, F: int, r: int) -> float | None:
     return a
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_llama1b_fwd_bwd.txt")
+
+
+def kernel_sources_sha256() -> str:
+    """sha256 over the HIP sources (file name then content, sorted by name)."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2605_03667_amd", "csrc", "*"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(tag: str):
+    """(read bytes, write bytes) per launch of a kernel tag from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE summary (copy-calibrated), or None when
+    the kernel sources changed since the counters were taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    sha, rows = None, {}
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            if line.startswith("kernel_sources_sha256:"):
+                sha = line.split(":", 1)[1].strip()
+            parts = [x.strip() for x in line.split("|")]
+            if len(parts) >= 5 and parts[3].isdigit() and parts[4].isdigit():
+                for t in parts[0].split(","):
+                    rows[t.strip()] = (int(parts[3]), int(parts[4]))
+    if sha != kernel_sources_sha256():
+        return None
+    return rows.get(tag)
+
+
 def cpu_baseline(cfg: dict, sample_tokens: int) -> dict:
     import numpy as np
     from threadpoolctl import threadpool_info
@@ -87,6 +122,8 @@ def main() -> int:
     ap.add_argument("--workload", default="llama1b")
     ap.add_argument("--cpu-sample", type=int, default=16384, help="tokens for the CPU oracle baseline (0: skip)")
     ap.add_argument("--no-sparsify", action="store_true", help="skip the standalone sparsify measurement")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (known traffic) for HBM counter calibration")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (--gpus {args.gpus} requested): the ELAS FFN path here is "
@@ -169,9 +206,14 @@ def main() -> int:
     dom_avg_s = kernels[dom][1] / kernels[dom][0] / 1e3
     dom_alg = algorithmic_flops(dom, T, d, F, r)
     achieved = dom_alg / dom_avg_s / 1e12
+    tr = measured_traffic(dom) if args.workload == "llama1b" else None
     roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": None if tr is None else tr[0] + tr[1],
                 "alg_flop_per_launch": dom_alg, "avg_us": round(dom_avg_s * 1e6, 2)}
+    if tr is not None:
+        roofline["traffic_read_bytes"], roofline["traffic_write_bytes"] = tr
+        roofline["traffic_source"] = os.path.relpath(TRAFFIC_FILE, ROOT)
 
     sp_tag = "k3_spmm_down"
     sp_avg_s = kernels[sp_tag][1] / kernels[sp_tag][0] / 1e3
@@ -214,6 +256,17 @@ def main() -> int:
         result["sparsify"] = {"shape": [M, N], "avg_us": round(avg_s * 1e6, 2), "alg_bytes": alg_bytes,
                               "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                               "frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+    if args.copy_calibration:
+        # a plain copy of known size: reads 1 GiB and writes 1 GiB per launch
+        src = torch.empty(1 << 29, dtype=torch.int16, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        result["copy_calibration"] = {"bytes_read": src.numel() * 2, "bytes_written": dst.numel() * 2,
+                                      "launches": 5}
+        del src, dst
 
     if args.cpu_sample > 0:
         print(f"[bench] cpu oracle on {args.cpu_sample} tokens", file=sys.stderr, flush=True)

@@ -77,8 +77,11 @@ struct GemmArgs {
 };
 
 template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int AMODE_, int BMODE_, int EPI_, bool M_FAST_,
-          int STAGES_ = 2, bool SPREAD_ = false>
+          int STAGES_ = 2, bool SPREAD_ = false, bool PIPE_ = true>
 struct GemmCfg {
+  // PIPE: double-buffer the MFMA fragments (read sub-step kk+1 during kk's
+  // MFMAs); off saves registers.
+  static constexpr bool PIPE = PIPE_;
   // SPREAD: issue the next stage's loads in four parts between the MFMA
   // sub-steps instead of all at the start of a step.
   static constexpr bool SPREAD = SPREAD_;
@@ -378,11 +381,15 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           bfr[slot][j] = *(const bf16x8*)(lB + row * 128 + swz(row, 2 * kk + lhalf) * 16);
         }
       };
-      read(0, 0);
+      if constexpr (Cfg::PIPE) read(0, 0);
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {       // four k16 MFMA steps per 64-wide K step
-        const int cur = kk & 1;
-        if (kk + 1 < 4) read(kk + 1, cur ^ 1);
+        const int cur = Cfg::PIPE ? (kk & 1) : 0;
+        if constexpr (Cfg::PIPE) {
+          if (kk + 1 < 4) read(kk + 1, cur ^ 1);
+        } else {
+          read(kk, 0);
+        }
         hook(kk);
 #pragma unroll
         for (int i = 0; i < FM; ++i)
