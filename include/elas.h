@@ -70,6 +70,16 @@ extern "C" {
 #define ELAS_SPARSIFY_RELU2  0u /* s = max(0,h)^2 is ranked and stored (ELAS's activation) */
 #define ELAS_SPARSIFY_RAW    1u /* h itself is ranked by |h| and stored unchanged          */
 
+/* elas_lowrank_ffn_fwd / _bwd: activation mode (both calls must agree). */
+#define ELAS_MODE_SPARSE24   0u /* the ReLU^2 output is pruned to 2:4 and stored compressed    */
+#define ELAS_MODE_DENSE      2u /* dense activations, no selection (the paper's dense warm-up,
+                                   Sec. 3.4 and Algorithm 2; also the dense comparison run)   */
+/* elas_lowrank_ffn_bwd only: gradient through the 2:4 selection. */
+#define ELAS_BWD_STE         4u /* straight-through estimator of Eq. 4: the selection is the
+                                   identity in the backward, dH = dS * 2 relu(h) everywhere
+                                   (relu(h) recomputed from P and V_up); default is the
+                                   masked derivative dH = dS * mask * 2 relu(h)               */
+
 /* elas_spmm_24: layout of the dense operand B. */
 #define ELAS_B_KN            0  /* B is [K x N] row-major                         */
 #define ELAS_B_NK            1  /* B is [N x K] row-major (B^T stored)            */
@@ -128,18 +138,20 @@ int elas_spmm_24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, int64
  * Outputs (bf16, device, written):
  *   y      [T,d]
  *   P      [T,r]   saved for the backward (P = x U_up, rounded to bf16)
- *   s_vals [T x elas_vals_ld(d_ff)]  compressed S (kept s rounded to bf16)
- *   s_meta [T x elas_meta_ld(d_ff)]  its 2-bit indices
+ *   s_vals sparse mode: [T x elas_vals_ld(d_ff)] compressed S (kept s in bf16)
+ *          dense mode:  [T x d_ff] dense S = relu(H)^2 in bf16
+ *   s_meta sparse mode: [T x elas_meta_ld(d_ff)] 2-bit indices; dense mode:
+ *          not used (may be NULL)
  *   Z      [T,r]   saved for the backward
  * Rounding points: P, H (before ReLU^2), the kept s, Z and y are rounded to
  * bf16 (nearest-even); every product accumulates in fp32.  The 2:4 selection
  * ranks max(0, bf16(H))^2 exactly, ties to the lower index.
- * workspace >= elas_lowrank_ffn_fwd_workspace_bytes(T, d, d_ff, r).
- * flags must be 0.
+ * flags: ELAS_MODE_SPARSE24 (0) or ELAS_MODE_DENSE.
+ * workspace >= elas_lowrank_ffn_fwd_workspace_bytes(T, d, d_ff, r, flags).
  * Requires T >= 0, d, d_ff, r > 0, multiples of 8 and at most 65536.  T == 0 is
  * a no-op (pointers are then not inspected and may be NULL).
  */
-size_t elas_lowrank_ffn_fwd_workspace_bytes(int64_t T, int64_t d, int64_t d_ff, int64_t r);
+size_t elas_lowrank_ffn_fwd_workspace_bytes(int64_t T, int64_t d, int64_t d_ff, int64_t r, uint32_t flags);
 int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t* V_up,
                          const uint16_t* U_down, const uint16_t* V_down,
                          int64_t T, int64_t d, int64_t d_ff, int64_t r, uint32_t flags,
@@ -150,20 +162,25 @@ int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t
  * elas_lowrank_ffn_bwd -- backward of the block (Sec. 3.3.2, Sec. 3.4).
  *
  * dy [T,d] bf16 is dL/dY; x, U_up, V_up, U_down, V_down as in the forward;
- * P, s_vals, s_meta, Z are the forward's saved outputs (read only).
+ * P, s_vals, s_meta, Z are the forward's saved outputs (read only; s_meta
+ * unused in dense mode).
  * Outputs: dx [T,d] bf16 (written); dU_up [d,r], dV_up [r,d_ff],
  *   dU_down [d_ff,r], dV_down [r,d] fp32 (overwritten, not accumulated).
- * Gradient through the activation: dH = dS * mask * 2 relu(H) with the stored
- * mask, the derivative of the sparsified forward (relu(H) is recovered
- * exactly from the stored bf16 s).  The full-width activation is never read:
- * dU_down = S^T dZ uses the compressed S.
- * Rounding points: dZ, dH (kept entries), dP and dx are rounded to bf16.
- * workspace >= elas_lowrank_ffn_bwd_workspace_bytes(T, d, d_ff, r).
- * flags must be 0.  Same size rules as the forward; T == 0 writes zero
- * weight gradients (only the four gradient pointers and the workspace are
- * then inspected).
+ * Gradient through the activation:
+ *   default (sparse mode): dH = dS * mask * 2 relu(h) with the stored mask,
+ *     the derivative of the sparsified forward; relu(h) is recovered exactly
+ *     from the stored bf16 s.  The full-width activation is never read:
+ *     dU_down = S^T dZ and dV_up = P^T dH use the compressed form.
+ *   ELAS_BWD_STE (after a sparse forward): Eq. 4, dH = dS * 2 relu(h) at every
+ *     position; relu(h) is recomputed from P and V_up.
+ *   ELAS_MODE_DENSE (after a dense forward): dH = dS * 2 relu(h), dense.
+ * Rounding points: dZ, dH, dP and dx are rounded to bf16.
+ * flags: 0, ELAS_BWD_STE or ELAS_MODE_DENSE (the forward's mode).
+ * workspace >= elas_lowrank_ffn_bwd_workspace_bytes(T, d, d_ff, r, flags).
+ * Same size rules as the forward; T == 0 writes zero weight gradients (only
+ * the four gradient pointers and the workspace are then inspected).
  */
-size_t elas_lowrank_ffn_bwd_workspace_bytes(int64_t T, int64_t d, int64_t d_ff, int64_t r);
+size_t elas_lowrank_ffn_bwd_workspace_bytes(int64_t T, int64_t d, int64_t d_ff, int64_t r, uint32_t flags);
 int elas_lowrank_ffn_bwd(const uint16_t* dy, const uint16_t* x, const uint16_t* U_up,
                          const uint16_t* V_up, const uint16_t* U_down, const uint16_t* V_down,
                          int64_t T, int64_t d, int64_t d_ff, int64_t r, uint32_t flags,

@@ -22,7 +22,8 @@ __all__ = [
     "elas_spmm_24_workspace_bytes", "elas_lowrank_ffn_fwd", "elas_lowrank_ffn_fwd_workspace_bytes",
     "elas_lowrank_ffn_bwd", "elas_lowrank_ffn_bwd_workspace_bytes",
     "elas_timing_enable", "elas_timing_collect",
-    "ELAS_SPARSIFY_RELU2", "ELAS_SPARSIFY_RAW", "ELAS_B_KN", "ELAS_B_NK",
+    "ELAS_SPARSIFY_RELU2", "ELAS_SPARSIFY_RAW", "ELAS_B_KN", "ELAS_B_NK", "ELAS_MODE_SPARSE24",
+    "ELAS_MODE_DENSE", "ELAS_BWD_STE",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libelas.so")
@@ -31,6 +32,9 @@ ELAS_SPARSIFY_RELU2 = 0
 ELAS_SPARSIFY_RAW = 1
 ELAS_B_KN = 0
 ELAS_B_NK = 1
+ELAS_MODE_SPARSE24 = 0
+ELAS_MODE_DENSE = 2
+ELAS_BWD_STE = 4
 
 _STATUS = {0: "ELAS_OK", 1: "ELAS_ERR_NULL", 2: "ELAS_ERR_SHAPE", 3: "ELAS_ERR_ALIGN",
            4: "ELAS_ERR_WORKSPACE", 5: "ELAS_ERR_FLAGS", 6: "ELAS_ERR_DEVICE"}
@@ -57,9 +61,9 @@ _SIGNATURES = {
     "elas_sparsify_24": ([_p, _i64, _i64, _u32, _p, _p, _p], ctypes.c_int),
     "elas_spmm_24_workspace_bytes": ([_i64, _i64, _i64, ctypes.c_int], _sz),
     "elas_spmm_24": ([_p, _p, _i64, _i64, _p, _i64, ctypes.c_int, _p, _p, _sz, _p], ctypes.c_int),
-    "elas_lowrank_ffn_fwd_workspace_bytes": ([_i64, _i64, _i64, _i64], _sz),
+    "elas_lowrank_ffn_fwd_workspace_bytes": ([_i64, _i64, _i64, _i64, _u32], _sz),
     "elas_lowrank_ffn_fwd": ([_p] * 5 + [_i64] * 4 + [_u32] + [_p] * 5 + [_p, _sz, _p], ctypes.c_int),
-    "elas_lowrank_ffn_bwd_workspace_bytes": ([_i64, _i64, _i64, _i64], _sz),
+    "elas_lowrank_ffn_bwd_workspace_bytes": ([_i64, _i64, _i64, _i64, _u32], _sz),
     "elas_lowrank_ffn_bwd": ([_p] * 6 + [_i64] * 4 + [_u32] + [_p] * 4 + [_p] * 5 + [_p, _sz, _p],
                              ctypes.c_int),
     "elas_timing_enable": ([ctypes.c_int], ctypes.c_int),
@@ -156,30 +160,34 @@ def elas_spmm_24(a_vals: torch.Tensor, a_meta: torch.Tensor, K: int, b: torch.Te
     return c
 
 
-def elas_lowrank_ffn_fwd_workspace_bytes(T: int, d: int, d_ff: int, r: int) -> int:
-    return lib().elas_lowrank_ffn_fwd_workspace_bytes(T, d, d_ff, r)
+def elas_lowrank_ffn_fwd_workspace_bytes(T: int, d: int, d_ff: int, r: int, flags: int = 0) -> int:
+    return lib().elas_lowrank_ffn_fwd_workspace_bytes(T, d, d_ff, r, flags)
 
 
-def elas_lowrank_ffn_bwd_workspace_bytes(T: int, d: int, d_ff: int, r: int) -> int:
-    return lib().elas_lowrank_ffn_bwd_workspace_bytes(T, d, d_ff, r)
+def elas_lowrank_ffn_bwd_workspace_bytes(T: int, d: int, d_ff: int, r: int, flags: int = 0) -> int:
+    return lib().elas_lowrank_ffn_bwd_workspace_bytes(T, d, d_ff, r, flags)
 
 
 def elas_lowrank_ffn_fwd(x, U_up, V_up, U_down, V_down, flags: int = 0, out: dict | None = None,
                          workspace: torch.Tensor | None = None) -> dict:
-    """Forward of the low-rank 2:4 FFN.  Returns dict(y, P, s_vals, s_meta, Z)."""
+    """Forward of the low-rank 2:4 FFN.  Returns dict(y, P, s_vals, s_meta, Z).
+
+    With ``flags=ELAS_MODE_DENSE`` s_vals is the dense [T, d_ff] activation and
+    s_meta is None."""
     T, d = x.shape
     r = U_up.shape[1]
     F = V_up.shape[1]
     dev = x.device
+    dense = bool(flags & ELAS_MODE_DENSE)
     if out is None:
         out = {
             "y": torch.empty((T, d), dtype=torch.bfloat16, device=dev),
             "P": torch.empty((T, r), dtype=torch.bfloat16, device=dev),
-            "s_vals": torch.empty((T, elas_vals_ld(F)), dtype=torch.bfloat16, device=dev),
-            "s_meta": torch.empty((T, elas_meta_ld(F)), dtype=torch.uint8, device=dev),
+            "s_vals": torch.empty((T, F if dense else elas_vals_ld(F)), dtype=torch.bfloat16, device=dev),
+            "s_meta": None if dense else torch.empty((T, elas_meta_ld(F)), dtype=torch.uint8, device=dev),
             "Z": torch.empty((T, r), dtype=torch.bfloat16, device=dev),
         }
-    need = elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r)
+    need = elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r, flags)
     if workspace is None:
         workspace = _workspace(need, dev)
     bf = torch.bfloat16
@@ -196,7 +204,10 @@ def elas_lowrank_ffn_fwd(x, U_up, V_up, U_down, V_down, flags: int = 0, out: dic
 def elas_lowrank_ffn_bwd(dy, x, U_up, V_up, U_down, V_down, saved: dict, flags: int = 0,
                          grads: dict | None = None, workspace: torch.Tensor | None = None) -> dict:
     """Backward of the low-rank 2:4 FFN given the forward's saved tensors
-    (P, s_vals, s_meta, Z).  Returns dict(dx, dU_up, dV_up, dU_down, dV_down)."""
+    (P, s_vals, s_meta, Z).  Returns dict(dx, dU_up, dV_up, dU_down, dV_down).
+
+    flags: 0 (masked derivative), ELAS_BWD_STE (Eq. 4 straight-through) or
+    ELAS_MODE_DENSE (after a dense forward)."""
     T, d = x.shape
     r = U_up.shape[1]
     F = V_up.shape[1]
@@ -210,7 +221,7 @@ def elas_lowrank_ffn_bwd(dy, x, U_up, V_up, U_down, V_down, saved: dict, flags: 
             "dU_down": torch.empty((F, r), dtype=f32, device=dev),
             "dV_down": torch.empty((r, d), dtype=f32, device=dev),
         }
-    need = elas_lowrank_ffn_bwd_workspace_bytes(T, d, F, r)
+    need = elas_lowrank_ffn_bwd_workspace_bytes(T, d, F, r, flags)
     if workspace is None:
         workspace = _workspace(need, dev)
     bf, f32 = torch.bfloat16, torch.float32

@@ -129,9 +129,9 @@ int elas_spmm_24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, int64
                        "spmm launch");
 }
 
-size_t elas_lowrank_ffn_fwd_workspace_bytes(int64_t T, int64_t d, int64_t d_ff, int64_t r) {
+size_t elas_lowrank_ffn_fwd_workspace_bytes(int64_t T, int64_t d, int64_t d_ff, int64_t r, uint32_t flags) {
   if (T < 0 || d <= 0 || d_ff <= 0 || r <= 0) return 0;
-  return elas::fwd_workspace_bytes(T, d, d_ff, r);
+  return elas::fwd_workspace_bytes(T, d, d_ff, r, (flags & ELAS_MODE_DENSE) != 0);
 }
 
 int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t* V_up, const uint16_t* U_down,
@@ -139,7 +139,8 @@ int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t
                          uint16_t* y, uint16_t* P, uint16_t* s_vals, uint8_t* s_meta, uint16_t* Z,
                          void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
-  if (flags != 0) return fail(ELAS_ERR_FLAGS, "flags must be 0");
+  if (flags & ~ELAS_MODE_DENSE) return fail(ELAS_ERR_FLAGS, "forward flags: only ELAS_MODE_DENSE is allowed");
+  const bool dense = (flags & ELAS_MODE_DENSE) != 0;
   ELAS_CHECK(check_ffn_dims(T, d, d_ff, r));
   if (T == 0) return ELAS_OK;
   ELAS_CHECK(check_ptr(x, "x"));
@@ -150,9 +151,9 @@ int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t
   ELAS_CHECK(check_ptr(y, "y"));
   ELAS_CHECK(check_ptr(P, "P"));
   ELAS_CHECK(check_ptr(s_vals, "s_vals"));
-  ELAS_CHECK(check_ptr(s_meta, "s_meta"));
+  if (!dense) ELAS_CHECK(check_ptr(s_meta, "s_meta"));
   ELAS_CHECK(check_ptr(Z, "Z"));
-  const size_t need = elas::fwd_workspace_bytes(T, d, d_ff, r);
+  const size_t need = elas::fwd_workspace_bytes(T, d, d_ff, r, dense);
   if (workspace_bytes < need)
     return fail(ELAS_ERR_WORKSPACE, "workspace %zu bytes, %zu needed", workspace_bytes, need);
   if (need) ELAS_CHECK(check_ptr(workspace, "workspace"));
@@ -161,12 +162,13 @@ int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t
   a.x = x; a.U_up = U_up; a.V_up = V_up; a.U_down = U_down; a.V_down = V_down;
   a.y = y; a.P = P; a.P_in = P; a.s_vals = s_vals; a.s_meta = s_meta; a.Z = Z;
   a.ws = workspace;
+  a.dense = dense;
   return device_status(elas::run_fwd(a, (hipStream_t)stream), "forward launch");
 }
 
-size_t elas_lowrank_ffn_bwd_workspace_bytes(int64_t T, int64_t d, int64_t d_ff, int64_t r) {
+size_t elas_lowrank_ffn_bwd_workspace_bytes(int64_t T, int64_t d, int64_t d_ff, int64_t r, uint32_t flags) {
   if (T < 0 || d <= 0 || d_ff <= 0 || r <= 0) return 0;
-  return elas::bwd_workspace_bytes(T, d, d_ff, r);
+  return elas::bwd_workspace_bytes(T, d, d_ff, r, (flags & ELAS_MODE_DENSE) != 0, (flags & ELAS_BWD_STE) != 0);
 }
 
 int elas_lowrank_ffn_bwd(const uint16_t* dy, const uint16_t* x, const uint16_t* U_up, const uint16_t* V_up,
@@ -175,7 +177,10 @@ int elas_lowrank_ffn_bwd(const uint16_t* dy, const uint16_t* x, const uint16_t* 
                          const uint8_t* s_meta, const uint16_t* Z, uint16_t* dx, float* dU_up, float* dV_up,
                          float* dU_down, float* dV_down, void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
-  if (flags != 0) return fail(ELAS_ERR_FLAGS, "flags must be 0");
+  if (flags & ~(ELAS_MODE_DENSE | ELAS_BWD_STE))
+    return fail(ELAS_ERR_FLAGS, "backward flags: only ELAS_MODE_DENSE or ELAS_BWD_STE are allowed");
+  const bool dense = (flags & ELAS_MODE_DENSE) != 0, ste = (flags & ELAS_BWD_STE) != 0;
+  if (dense && ste) return fail(ELAS_ERR_FLAGS, "ELAS_BWD_STE applies to the sparse forward only");
   ELAS_CHECK(check_ffn_dims(T, d, d_ff, r));
   if (T > 0) {   // with no tokens only the weight gradients (zeros) are written
     ELAS_CHECK(check_ptr(dy, "dy"));
@@ -186,7 +191,7 @@ int elas_lowrank_ffn_bwd(const uint16_t* dy, const uint16_t* x, const uint16_t* 
     ELAS_CHECK(check_ptr(V_down, "V_down"));
     ELAS_CHECK(check_ptr(P, "P"));
     ELAS_CHECK(check_ptr(s_vals, "s_vals"));
-    ELAS_CHECK(check_ptr(s_meta, "s_meta"));
+    if (!dense) ELAS_CHECK(check_ptr(s_meta, "s_meta"));
     ELAS_CHECK(check_ptr(Z, "Z"));
     ELAS_CHECK(check_ptr(dx, "dx"));
   }
@@ -194,7 +199,7 @@ int elas_lowrank_ffn_bwd(const uint16_t* dy, const uint16_t* x, const uint16_t* 
   ELAS_CHECK(check_ptr(dV_up, "dV_up"));
   ELAS_CHECK(check_ptr(dU_down, "dU_down"));
   ELAS_CHECK(check_ptr(dV_down, "dV_down"));
-  const size_t need = elas::bwd_workspace_bytes(T, d, d_ff, r);
+  const size_t need = elas::bwd_workspace_bytes(T, d, d_ff, r, dense, ste);
   if (workspace_bytes < need)
     return fail(ELAS_ERR_WORKSPACE, "workspace %zu bytes, %zu needed", workspace_bytes, need);
   if (need) ELAS_CHECK(check_ptr(workspace, "workspace"));
@@ -205,6 +210,8 @@ int elas_lowrank_ffn_bwd(const uint16_t* dy, const uint16_t* x, const uint16_t* 
   a.s_meta = const_cast<uint8_t*>(s_meta); a.Z = const_cast<uint16_t*>(Z);
   a.dy = dy; a.dx = dx; a.dU_up = dU_up; a.dV_up = dV_up; a.dU_down = dU_down; a.dV_down = dV_down;
   a.ws = workspace;
+  a.dense = dense;
+  a.ste = ste;
   return device_status(elas::run_bwd(a, (hipStream_t)stream), "backward launch");
 }
 

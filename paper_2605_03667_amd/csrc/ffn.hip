@@ -190,21 +190,31 @@ FwdWs fwd_ws(char* p, int64_t d, int64_t F, int64_t r) {
 }
 
 struct BwdWs {
-  uint16_t *dZ, *dH, *dP;
+  uint16_t *dZ, *dH, *dP, *R, *V_upT;
   float* part;
   size_t bytes;
 };
-BwdWs bwd_ws(char* p, int64_t T, int64_t d, int64_t F, int64_t r) {
+// dH is compressed [T x ldv] in the sparse backward and dense [T x F] in the
+// dense and straight-through ones; the straight-through backward also holds
+// the recomputed dense relu(h) [T x F] and V_up^T.
+BwdWs bwd_ws(char* p, int64_t T, int64_t d, int64_t F, int64_t r, bool dense, bool ste) {
   const int64_t Fp = pad64(F);
   Carver c{p};
-  BwdWs w;
+  BwdWs w{};
   w.dZ = c.take<uint16_t>(T * r);
-  w.dH = c.take<uint16_t>(T * vals_ld(F));
+  w.dH = c.take<uint16_t>(T * ((dense || ste) ? F : vals_ld(F)));
   w.dP = c.take<uint16_t>(T * r);
+  if (ste) {
+    w.R = c.take<uint16_t>(T * F);
+    w.V_upT = c.take<uint16_t>(Fp * r);
+  }
+  // split-K partials of the products over tokens (d_ff-wide ones have Fp rows
+  // when read compressed, F rows when dense)
   size_t pb = partial_bytes(r, d, T);
-  const size_t p2 = partial_bytes(Fp, r, T), p3 = partial_bytes(d, r, T);
+  const size_t p2 = partial_bytes(Fp, r, T), p3 = partial_bytes(d, r, T), p4 = partial_bytes(F, r, T);
   if (p2 > pb) pb = p2;
   if (p3 > pb) pb = p3;
+  if (p4 > pb) pb = p4;
   w.part = c.take<float>(pb / sizeof(float));
   w.bytes = c.used;
   return w;
@@ -222,13 +232,14 @@ size_t spmm_workspace_bytes(int64_t K, int64_t N, int b_layout) {
   return b_layout == 0 ? align_up((size_t)K * N * sizeof(uint16_t)) : 0;
 }
 
-size_t fwd_workspace_bytes(int64_t T, int64_t d, int64_t F, int64_t r) {
+size_t fwd_workspace_bytes(int64_t T, int64_t d, int64_t F, int64_t r, bool dense) {
   (void)T;
+  (void)dense;
   return fwd_ws(nullptr, d, F, r).bytes;
 }
 
-size_t bwd_workspace_bytes(int64_t T, int64_t d, int64_t F, int64_t r) {
-  return bwd_ws(nullptr, T, d, F, r).bytes;
+size_t bwd_workspace_bytes(int64_t T, int64_t d, int64_t F, int64_t r, bool dense, bool ste) {
+  return bwd_ws(nullptr, T, d, F, r, dense, ste).bytes;
 }
 
 hipError_t run_spmm24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, int64_t K, const uint16_t* b,
@@ -259,22 +270,28 @@ hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
   ELAS_TRY(transpose_pad(a.V_down, r, d, d, w.V_downT, d, r, r, st));      // [d x r]
   // P = x U_up
   ELAS_TRY(gemm_nt_bf16("k1_up_gemm", a.x, d, w.U_upT, d, a.P, r, T, r, d, st));
-  // H^T = V_up^T P^T with ReLU^2 + 2:4 selection + compression in the epilogue
-  {
+  if (!a.dense) {
+    // H^T = V_up^T P^T with ReLU^2 + 2:4 selection + compression in the epilogue
     GemmArgs g{};
     g.A = w.V_upT; g.lda = r; g.B = a.P; g.ldb = r;
     g.M = Fp; g.N = T; g.K = r; g.m_valid = Fp; g.ka_valid = r; g.kb_valid = r;
     g.sv = a.s_vals; g.sm = a.s_meta; g.ldv = vals_ld(F); g.ldm = meta_ld(F);
     ELAS_TRY(launch<CfgNT<256, EPI_SPARSIFY, true>>("k2_up_relu2_sparsify", g, 1, st));
-  }
-  // Z = S U_down on the 2:4 operand
-  {
+    // Z = S U_down on the 2:4 operand
+    GemmArgs z{};
+    z.A = a.s_vals; z.lda = vals_ld(F); z.Am = a.s_meta; z.ldam = meta_ld(F);
+    z.B = w.U_downT; z.ldb = Fp;
+    z.M = T; z.N = r; z.K = Fp; z.m_valid = T; z.ka_valid = Fp; z.kb_valid = Fp;
+    z.C = a.Z; z.ldc = r;
+    ELAS_TRY(launch<CfgSP>("k3_spmm_down", z, 1, st));
+  } else {
+    // dense activations: S = relu(H)^2 written [T x F], then a dense product
     GemmArgs g{};
-    g.A = a.s_vals; g.lda = vals_ld(F); g.Am = a.s_meta; g.ldam = meta_ld(F);
-    g.B = w.U_downT; g.ldb = Fp;
-    g.M = T; g.N = r; g.K = Fp; g.m_valid = T; g.ka_valid = Fp; g.kb_valid = Fp;
-    g.C = a.Z; g.ldc = r;
-    ELAS_TRY(launch<CfgSP>("k3_spmm_down", g, 1, st));
+    g.A = w.V_upT; g.lda = r; g.B = a.P; g.ldb = r;
+    g.M = Fp; g.N = T; g.K = r; g.m_valid = Fp; g.ka_valid = r; g.kb_valid = r;
+    g.act = a.s_vals; g.ld_act = F; g.f_valid = F; g.act_square = 1;
+    ELAS_TRY(launch<CfgNT<256, EPI_ACT_DENSE, true>>("k2_up_relu2_dense", g, 1, st));
+    ELAS_TRY(gemm_nt_bf16("k3_down_gemm_dense", a.s_vals, F, w.U_downT, Fp, a.Z, r, T, r, F, st));
   }
   // Y = Z V_down
   ELAS_TRY(gemm_nt_bf16("k4_down_gemm", a.Z, r, w.V_downT, r, a.y, d, T, d, r, st));
@@ -291,33 +308,66 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
     ELAS_TRY(fill_zero(a.dV_down, r * d, st));
     return hipSuccess;
   }
-  const BwdWs w = bwd_ws((char*)a.ws, T, d, F, r);
+  const BwdWs w = bwd_ws((char*)a.ws, T, d, F, r, a.dense, a.ste);
   // dZ = dY V_down^T   (V_down [r x d] is already the K-contiguous operand)
   ELAS_TRY(gemm_nt_bf16("b1_dZ", a.dy, d, a.V_down, d, w.dZ, r, T, r, d, st));
   // dV_down = Z^T dY
   ELAS_TRY(gemm_tt_f32<OP_T>("b2_dV_down", a.Z, r, nullptr, 0, a.dy, d, r, d, T, w.part, a.dV_down, r, false, d, st));
-  // dH = (dZ U_down^T) * mask * 2 relu(H), computed as dS^T = U_down dZ^T
-  {
+  if (!a.dense && !a.ste) {
+    // dH = (dZ U_down^T) * mask * 2 relu(H), computed as dS^T = U_down dZ^T
     GemmArgs g{};
     g.A = a.U_down; g.lda = r; g.B = w.dZ; g.ldb = r;
     g.M = Fp; g.N = T; g.K = r; g.m_valid = F; g.ka_valid = r; g.kb_valid = r;
     g.sv = a.s_vals; g.sm = a.s_meta; g.ldv = ldv; g.ldm = ldm; g.dv = w.dH;
     ELAS_TRY(launch<CfgNT<256, EPI_DH, true>>("b3_dH_masked", g, 1, st));
-  }
-  // dU_down = S^T dZ from the compressed S
-  ELAS_TRY(gemm_tt_f32<OP_TSP>("b4_dU_down", a.s_vals, ldv, a.s_meta, ldm, w.dZ, r, Fp, r, T, w.part, a.dU_down, F, false, r,
-                               st));
-  // dP = dH V_up^T on the 2:4 operand (V_up [r x F] is already K-contiguous)
-  {
+    // dU_down = S^T dZ from the compressed S
+    ELAS_TRY(gemm_tt_f32<OP_TSP>("b4_dU_down", a.s_vals, ldv, a.s_meta, ldm, w.dZ, r, Fp, r, T, w.part, a.dU_down, F,
+                                 false, r, st));
+    // dP = dH V_up^T on the 2:4 operand (V_up [r x F] is already K-contiguous)
+    GemmArgs p{};
+    p.A = w.dH; p.lda = ldv; p.Am = a.s_meta; p.ldam = ldm;
+    p.B = a.V_up; p.ldb = F;
+    p.M = T; p.N = r; p.K = Fp; p.m_valid = T; p.ka_valid = Fp; p.kb_valid = F;
+    p.C = w.dP; p.ldc = r;
+    ELAS_TRY(launch<CfgSP>("b5_spmm_dP", p, 1, st));
+    // dV_up = P^T dH, computed as dV_up^T = dH^T P and written transposed
+    ELAS_TRY(gemm_tt_f32<OP_TSP>("b6_dV_up", w.dH, ldv, a.s_meta, ldm, a.P_in, r, Fp, r, T, w.part, a.dV_up, F, true, F,
+                                 st));
+  } else {
+    // dense dH [T x F] = dS * 2 r at every position: r = bf16(sqrt(s)) from the
+    // dense S (dense mode), or relu(h) recomputed from P and V_up (straight-
+    // through estimator of Eq. 4 after a sparse forward)
+    const uint16_t* act = a.s_vals;
+    int square = 1;
+    if (a.ste) {
+      ELAS_TRY(transpose_pad(a.V_up, r, F, F, w.V_upT, Fp, r, r, st));      // [Fp x r], zero rows >= F
+      GemmArgs h{};
+      h.A = w.V_upT; h.lda = r; h.B = a.P_in; h.ldb = r;
+      h.M = Fp; h.N = T; h.K = r; h.m_valid = Fp; h.ka_valid = r; h.kb_valid = r;
+      h.act = w.R; h.ld_act = F; h.f_valid = F; h.act_square = 0;
+      ELAS_TRY(launch<CfgNT<256, EPI_ACT_DENSE, true>>("b3_relu_h_recompute", h, 1, st));
+      act = w.R;
+      square = 0;
+    }
     GemmArgs g{};
-    g.A = w.dH; g.lda = ldv; g.Am = a.s_meta; g.ldam = ldm;
-    g.B = a.V_up; g.ldb = F;
-    g.M = T; g.N = r; g.K = Fp; g.m_valid = T; g.ka_valid = Fp; g.kb_valid = F;
-    g.C = w.dP; g.ldc = r;
-    ELAS_TRY(launch<CfgSP>("b5_spmm_dP", g, 1, st));
+    g.A = a.U_down; g.lda = r; g.B = w.dZ; g.ldb = r;
+    g.M = Fp; g.N = T; g.K = r; g.m_valid = F; g.ka_valid = r; g.kb_valid = r;
+    g.act = const_cast<uint16_t*>(act); g.ld_act = F; g.f_valid = F; g.act_square = square; g.dact = w.dH;
+    ELAS_TRY(launch<CfgNT<256, EPI_DH_DENSE, true>>(a.ste ? "b3_dH_ste" : "b3_dH_dense", g, 1, st));
+    if (a.dense) {
+      // dU_down = S^T dZ with the dense S
+      ELAS_TRY(gemm_tt_f32<OP_T>("b4_dU_down_dense", a.s_vals, F, nullptr, 0, w.dZ, r, F, r, T, w.part, a.dU_down, F,
+                                 false, r, st));
+    } else {
+      ELAS_TRY(gemm_tt_f32<OP_TSP>("b4_dU_down", a.s_vals, ldv, a.s_meta, ldm, w.dZ, r, Fp, r, T, w.part, a.dU_down,
+                                   F, false, r, st));
+    }
+    // dP = dH V_up^T (dense)
+    ELAS_TRY(gemm_nt_bf16("b5_dP_dense", w.dH, F, a.V_up, F, w.dP, r, T, r, F, st));
+    // dV_up^T = dH^T P (dense), written transposed
+    ELAS_TRY(gemm_tt_f32<OP_T>("b6_dV_up_dense", w.dH, F, nullptr, 0, a.P_in, r, F, r, T, w.part, a.dV_up, F, true,
+                               F, st));
   }
-  // dV_up = P^T dH, computed as dV_up^T = dH^T P and written transposed
-  ELAS_TRY(gemm_tt_f32<OP_TSP>("b6_dV_up", w.dH, ldv, a.s_meta, ldm, a.P_in, r, Fp, r, T, w.part, a.dV_up, F, true, F, st));
   // dU_up = x^T dP
   ELAS_TRY(gemm_tt_f32<OP_T>("b7_dU_up", a.x, d, nullptr, 0, w.dP, r, d, r, T, w.part, a.dU_up, d, false, r, st));
   // dx = dP U_up^T   (U_up [d x r] is already K-contiguous)

@@ -52,7 +52,14 @@
 namespace elas {
 
 enum OpMode { OP_K = 0, OP_T = 1, OP_SP = 2, OP_TSP = 3 };
-enum EpiMode { EPI_BF16 = 0, EPI_F32 = 1, EPI_SPARSIFY = 2, EPI_DH = 3 };
+enum EpiMode {
+  EPI_BF16 = 0,       // C bf16
+  EPI_F32 = 1,        // fp32 split-K partials
+  EPI_SPARSIFY = 2,   // ReLU^2 + top-2 of 4 + compressed write (C = H^T)
+  EPI_DH = 3,         // dH = dS * mask * 2 relu(h), compressed (C = dS^T)
+  EPI_ACT_DENSE = 4,  // dense activation: relu(h)^2 (act_square) or relu(h) (C = H^T)
+  EPI_DH_DENSE = 5,   // dense dH = dS * 2 r, r from a dense activation (C = dS^T)
+};
 
 struct GemmArgs {
   const uint16_t* A;   // OP_K [M x K], OP_T [K x M], OP_SP vals [M x K/2], OP_TSP vals [K x M/2]
@@ -73,6 +80,13 @@ struct GemmArgs {
   uint8_t* sm;         // metadata of S [N x ldm]
   int64_t ldv, ldm;
   uint16_t* dv;        // EPI_DH: kept values of dH [N x ldv], written
+  // EPI_ACT_DENSE / EPI_DH_DENSE: dense [N x ld_act] activations (tokens as
+  // rows), features f < f_valid only.
+  uint16_t* act;       // ACT_DENSE: written; DH_DENSE: read (r = bf16(sqrt(a)) if act_square, else a)
+  uint16_t* dact;      // DH_DENSE: dense dH, written (pitch ld_act)
+  int64_t ld_act;
+  int64_t f_valid;
+  int act_square;
   int tiles_m, tiles_n;
 };
 
@@ -561,6 +575,72 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
               part[row * g.N + col] = acc[i][j][e];
             }
           }
+        }
+      }
+  } else if constexpr (Cfg::EPI == EPI_ACT_DENSE || Cfg::EPI == EPI_DH_DENSE) {
+    // C rows are features f, columns tokens t: accumulators 4b..4b+3 of a
+    // lane are features 8b + 4h + 0..3 of token column l % 32.  Lanes l and
+    // l+32 exchange halves so that each writes 16 contiguous features
+    // (half 0: 0..15, half 1: 16..31 of the 32-row block) of its token row.
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int64_t t = n0 + wn * TN + j * 32 + lrow;
+        const int64_t f32 = m0 + wm * TM + i * 32;
+        uint2 mine[4];   // block b: features f32 + 8b + 4h .. +3 as 4 bf16
+        if constexpr (Cfg::EPI == EPI_ACT_DENSE) {
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            uint32_t v[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const __bf16 hb = (__bf16)acc[i][j][4 * b + q];       // h rounded to bf16 (RNE)
+              const uint32_t r = relu_bits(__builtin_bit_cast(uint16_t, hb));
+              if (g.act_square) {
+                const float a = bf16_to_f32(r);
+                v[q] = f32_to_bf16_rne(a * a);
+              } else {
+                v[q] = r;
+              }
+            }
+            mine[b] = make_uint2(v[0] | (v[1] << 16), v[2] | (v[3] << 16));
+          }
+        } else {
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const int64_t f = f32 + 8 * b + 4 * lhalf;
+            uint2 a = make_uint2(0u, 0u);
+            if (t < g.N && f < g.f_valid) a = *(const uint2*)(g.act + t * g.ld_act + f);
+            const uint32_t av[4] = {a.x & 0xFFFFu, a.x >> 16, a.y & 0xFFFFu, a.y >> 16};
+            uint32_t v[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const float x = bf16_to_f32(av[q]);
+              const float r = g.act_square ? (float)(__bf16)__builtin_sqrtf(x) : x;
+              v[q] = __builtin_bit_cast(uint16_t, (__bf16)(acc[i][j][4 * b + q] * 2.0f * r));
+            }
+            mine[b] = make_uint2(v[0] | (v[1] << 16), v[2] | (v[3] << 16));
+          }
+        }
+        // half 0 needs the partner's blocks 0,1; half 1 the partner's 2,3
+        const uint2 give0 = lhalf ? mine[0] : mine[2];
+        const uint2 give1 = lhalf ? mine[1] : mine[3];
+        const uint2 got0 = make_uint2(__shfl_xor(give0.x, 32), __shfl_xor(give0.y, 32));
+        const uint2 got1 = make_uint2(__shfl_xor(give1.x, 32), __shfl_xor(give1.y, 32));
+        uint4 lo, hi;   // features +0..7 and +8..15 of this lane's 16
+        if (lhalf == 0) {
+          lo = make_uint4(mine[0].x, mine[0].y, got0.x, got0.y);
+          hi = make_uint4(mine[1].x, mine[1].y, got1.x, got1.y);
+        } else {
+          lo = make_uint4(got0.x, got0.y, mine[2].x, mine[2].y);
+          hi = make_uint4(got1.x, got1.y, mine[3].x, mine[3].y);
+        }
+        const int64_t f = f32 + 16 * lhalf;
+        if (t < g.N) {
+          uint16_t* dst = (Cfg::EPI == EPI_ACT_DENSE ? g.act : g.dact) + t * g.ld_act + f;
+          if (f + 8 <= g.f_valid) *(uint4*)dst = lo;
+          if (f + 16 <= g.f_valid) *(uint4*)(dst + 8) = hi;
         }
       }
   } else {

@@ -43,6 +43,8 @@ def test_binding_constants_match_header():
     assert d["ELAS_SPARSIFY_RELU2"] == elas.ELAS_SPARSIFY_RELU2
     assert d["ELAS_SPARSIFY_RAW"] == elas.ELAS_SPARSIFY_RAW
     assert d["ELAS_B_KN"] == elas.ELAS_B_KN and d["ELAS_B_NK"] == elas.ELAS_B_NK
+    assert d["ELAS_MODE_SPARSE24"] == elas.ELAS_MODE_SPARSE24 and d["ELAS_MODE_DENSE"] == elas.ELAS_MODE_DENSE
+    assert d["ELAS_BWD_STE"] == elas.ELAS_BWD_STE
     for k, v in elas._STATUS.items():
         assert d[v] == k
 
@@ -57,6 +59,9 @@ def test_pitches_and_workspace_sizes():
     assert w >= 2 * (512 * 2048 * 2 + 5504 * 512 * 2)
     wb = elas.elas_lowrank_ffn_bwd_workspace_bytes(65536, 2048, 5464, 512)
     assert wb >= 65536 * (512 * 2 * 2 + 2752 * 2)
+    wd = elas.elas_lowrank_ffn_bwd_workspace_bytes(65536, 2048, 5464, 512, elas.ELAS_MODE_DENSE)
+    ws = elas.elas_lowrank_ffn_bwd_workspace_bytes(65536, 2048, 5464, 512, elas.ELAS_BWD_STE)
+    assert wd >= 65536 * (512 * 2 * 2 + 5464 * 2) and ws >= wd + 65536 * 5464 * 2
     assert elas.elas_spmm_24_workspace_bytes(10, 64, 32, elas.ELAS_B_NK) == 0
     assert elas.elas_spmm_24_workspace_bytes(10, 64, 32, elas.ELAS_B_KN) >= 64 * 32 * 2
 
@@ -93,7 +98,7 @@ def test_spmm_validation():
 
 def _fwd(L, T=16, d=32, F=64, r=16, flags=0, ws=None, wsb=None, x=FAKE, y=FAKE):
     if wsb is None:
-        wsb = L.elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r)
+        wsb = L.elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r, flags)
     return L.elas_lowrank_ffn_fwd(x, FAKE, FAKE, FAKE, FAKE, T, d, F, r, flags, y, FAKE, FAKE, FAKE, FAKE,
                                   ws, wsb, None)
 
@@ -101,6 +106,7 @@ def _fwd(L, T=16, d=32, F=64, r=16, flags=0, ws=None, wsb=None, x=FAKE, y=FAKE):
 def test_fwd_validation():
     L = elas.lib()
     assert _fwd(L, flags=1) == 5
+    assert _fwd(L, flags=4) == 5                # STE is a backward-only flag
     assert _fwd(L, d=12) == 2
     assert _fwd(L, F=60) == 2
     assert _fwd(L, r=0) == 2
@@ -114,7 +120,7 @@ def test_fwd_validation():
 def test_bwd_validation():
     L = elas.lib()
     T, d, F, r = 16, 32, 64, 16
-    need = L.elas_lowrank_ffn_bwd_workspace_bytes(T, d, F, r)
+    need = L.elas_lowrank_ffn_bwd_workspace_bytes(T, d, F, r, 0)
 
     def call(**kw):
         a = dict(dy=FAKE, flags=0, d=d, ws=FAKE, wsb=need, dV_down=FAKE)
@@ -122,7 +128,8 @@ def test_bwd_validation():
         return L.elas_lowrank_ffn_bwd(a["dy"], FAKE, FAKE, FAKE, FAKE, FAKE, T, a["d"], F, r, a["flags"],
                                       FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, a["dV_down"],
                                       a["ws"], a["wsb"], None)
-    assert call(flags=4) == 5
+    assert call(flags=8) == 5                   # unknown bit
+    assert call(flags=6) == 5                   # STE needs the sparse forward
     assert call(d=20) == 2
     assert call(dy=None) == 1
     assert call(dV_down=MIS) == 3

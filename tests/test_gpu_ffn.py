@@ -30,12 +30,17 @@ TOL = 2e-2
 GRADS = ("dU_up", "dV_up", "dU_down", "dV_down")
 
 
-def run_gpu(bits, rows=None):
+def run_gpu(bits, rows=None, mode="sparse"):
     """Forward + backward through the C ABI; returns host copies (float64 for
-    numbers) of the outputs, restricted to the token rows ``rows`` if given."""
+    numbers) of the outputs, restricted to the token rows ``rows`` if given.
+    mode: "sparse" (default), "ste" (sparse forward, Eq. 4 backward) or
+    "dense" (dense activations)."""
+    fflags = elas.ELAS_MODE_DENSE if mode == "dense" else 0
+    bflags = {"sparse": 0, "ste": elas.ELAS_BWD_STE, "dense": elas.ELAS_MODE_DENSE}[mode]
     t = {k: dev_bf16(v) for k, v in bits.items()}
-    fwd = elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"])
-    bwd = elas.elas_lowrank_ffn_bwd(t["dY"], t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], fwd)
+    fwd = elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], flags=fflags)
+    bwd = elas.elas_lowrank_ffn_bwd(t["dY"], t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], fwd,
+                                    flags=bflags)
     torch.cuda.synchronize()
     del t
     F = bits["V_up"].shape[1]
@@ -47,15 +52,20 @@ def run_gpu(bits, rows=None):
     out = {
         "Y": obf.to_f64(host_bits(rows_of(fwd["y"]))), "P": obf.to_f64(host_bits(rows_of(fwd["P"]))),
         "Z": obf.to_f64(host_bits(rows_of(fwd["Z"]))), "dx": obf.to_f64(host_bits(rows_of(bwd["dx"]))),
-        "s_vals": host_bits(rows_of(fwd["s_vals"])), "s_meta": rows_of(fwd["s_meta"]).cpu().numpy(),
+        "s_vals": host_bits(rows_of(fwd["s_vals"])),
     }
     for k in GRADS:
         out[k] = bwd[k].cpu().numpy().astype(np.float64)
+    if mode == "dense":
+        out["S"] = obf.to_f64(out["s_vals"])
+        out["mask"] = np.ones(out["S"].shape, dtype=bool)
+    else:
+        out["s_meta"] = rows_of(fwd["s_meta"]).cpu().numpy()
+        check_padding(out["s_vals"], out["s_meta"], F)
+        dense, mask = osp.decompress(out["s_vals"][:, : F // 2], out["s_meta"][:, : F // 8], F)
+        out["mask"] = mask
+        out["S"] = obf.to_f64(dense)
     del fwd, bwd
-    check_padding(out["s_vals"], out["s_meta"], F)
-    dense, mask = osp.decompress(out["s_vals"][:, : F // 2], out["s_meta"][:, : F // 8], F)
-    out["mask"] = mask
-    out["S"] = obf.to_f64(dense)
     return out
 
 
@@ -185,3 +195,45 @@ def test_zero_tokens():
     torch.cuda.synchronize()
     for k in GRADS:
         assert torch.all(grads[k] == 0), k
+
+
+@pytest.mark.parametrize("mode", ["dense", "ste"])
+@pytest.mark.parametrize("T,d,F,r", [(5, 16, 24, 8), (700, 136, 1000, 72), (300, 512, 1376, 128),
+                                     (129, 2048, 5464, 512)])
+def test_modes_small(mode, T, d, F, r):
+    """Dense activations (the paper's warm-up phase) and the straight-through
+    backward of Eq. 4, against the oracle in the same mode."""
+    bits = ffn_inputs(T, d, F, r, seed_base=T + r)
+    f, b = offn.run(bits, sparse=(mode != "dense"), ste=(mode == "ste"))
+    gpu = run_gpu(bits, mode=mode)
+    compare(gpu, f, b)
+    if mode == "dense":
+        # same bf16 h on both sides except where fp32 and float64 accumulation
+        # of H straddle a bf16 rounding boundary (about 0.1 % at K = 512)
+        assert np.mean(gpu["S"] == f["S"]) > 0.995
+
+
+@pytest.mark.parametrize("mode", ["dense", "ste"])
+def test_modes_llama60m_full(mode):
+    bits = config_inputs("llama60m")
+    f, b = offn.run(bits, sparse=(mode != "dense"), ste=(mode == "ste"))
+    rep = {}
+    compare(run_gpu(bits, mode=mode), f, b, report=rep)
+    print(mode, rep)
+
+
+def test_ste_equals_masked_when_at_most_two_positives():
+    """When every group has <= 2 positive h, pruned slots have relu(h) = 0, so
+    the straight-through and masked backward agree (GPU vs GPU)."""
+    T, d, F, r = 300, 64, 136, 8
+    bits = ffn_inputs(T, d, F, r, seed_base=21)
+    # H = P V_up with P's column 0 > 0 only and V_up row 0 signed (+ + - -) per group
+    g = np.random.default_rng(5)
+    x = np.zeros((T, d), dtype=np.float32); x[:, 0] = np.abs(g.standard_normal(T)) + 0.1
+    U = np.zeros((d, r), dtype=np.float32); U[0, 0] = 1.0
+    V = np.zeros((r, F), dtype=np.float32); V[0] = np.tile([1, 1, -1, -1], F // 4) * (np.abs(g.standard_normal(F)) + 0.1)
+    to_bits = lambda a: (a.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    bits["x"], bits["U_up"], bits["V_up"] = to_bits(x), to_bits(U), to_bits(V)
+    a, s = run_gpu(bits, mode="sparse"), run_gpu(bits, mode="ste")
+    for k in ("dx",) + GRADS:
+        assert rel_fro(s[k], a[k]) < 1e-2, k
