@@ -96,6 +96,81 @@ def measured_traffic(tag: str):
     return rows.get(tag)
 
 
+def large_batch_compare(steps: int, warmup: int) -> dict:
+    """The 1B shape at T = 262144 tokens, 2:4-compressed vs dense activations:
+    tokens/s of forward + backward and activation memory.  `stored_bytes` are
+    the tensors the forward keeps for the backward (P, Z and S, compressed or
+    dense); `peak_bytes` is torch's allocator high-water mark above the inputs,
+    weights and gradients over one forward + backward, each call allocating
+    its workspace and freeing it afterwards."""
+    import numpy as np
+    import torch
+
+    import paper_2605_03667_amd as elas
+    from synthetic import CONFIGS, config_inputs
+
+    name = "llama1b_t262144"
+    cfg = CONFIGS[name]
+    T, d, F, r = cfg["T"], cfg["d"], cfg["d_ff"], cfg["r"]
+    dev = torch.device("cuda:0")
+    bits = config_inputs(name)
+    t = {k: torch.from_numpy(v.view(np.int16)).view(torch.bfloat16).to(dev) for k, v in bits.items()}
+    del bits
+    f32 = torch.float32
+    grads = {"dx": torch.empty((T, d), dtype=torch.bfloat16, device=dev),
+             "dU_up": torch.empty((d, r), dtype=f32, device=dev), "dV_up": torch.empty((r, F), dtype=f32, device=dev),
+             "dU_down": torch.empty((F, r), dtype=f32, device=dev),
+             "dV_down": torch.empty((r, d), dtype=f32, device=dev)}
+    out = {}
+    for mode, fflags, bflags in (("sparse_2to4", 0, 0), ("dense", elas.ELAS_MODE_DENSE, elas.ELAS_MODE_DENSE)):
+        torch.cuda.synchronize()
+        base = torch.cuda.memory_allocated(dev)
+        torch.cuda.reset_peak_memory_stats(dev)
+        ws = torch.empty(elas.elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r, fflags), dtype=torch.uint8, device=dev)
+        saved = elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], flags=fflags,
+                                          workspace=ws)
+        del ws
+        ws = torch.empty(elas.elas_lowrank_ffn_bwd_workspace_bytes(T, d, F, r, bflags), dtype=torch.uint8, device=dev)
+        elas.elas_lowrank_ffn_bwd(t["dY"], t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], saved,
+                                  flags=bflags, grads=grads, workspace=ws)
+        del ws
+        torch.cuda.synchronize()
+        peak = torch.cuda.max_memory_allocated(dev) - base
+        stored = {k: v.numel() * v.element_size() for k, v in saved.items() if k != "y" and v is not None}
+        ws_f = torch.empty(elas.elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r, fflags), dtype=torch.uint8,
+                           device=dev)
+        ws_b = torch.empty(elas.elas_lowrank_ffn_bwd_workspace_bytes(T, d, F, r, bflags), dtype=torch.uint8,
+                           device=dev)
+
+        def step():
+            elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], flags=fflags,
+                                      out=saved, workspace=ws_f)
+            elas.elas_lowrank_ffn_bwd(t["dY"], t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], saved,
+                                      flags=bflags, grads=grads, workspace=ws_b)
+
+        for _ in range(warmup):
+            step()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(steps):
+            step()
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / steps
+        out[mode] = {"tokens_per_s": round(T / (ms / 1e3), 1), "ms_per_step": round(ms, 3),
+                     "stored_bytes": sum(stored.values()), "stored_breakdown": stored, "peak_bytes": int(peak)}
+        del saved, ws_f, ws_b
+        torch.cuda.empty_cache()
+    sp, de = out["sparse_2to4"], out["dense"]
+    out["stored_ratio_sparse_over_dense"] = round(sp["stored_bytes"] / de["stored_bytes"], 4)
+    s_sp = sp["stored_breakdown"]["s_vals"] + sp["stored_breakdown"]["s_meta"]
+    out["activation_ratio_sparse_over_dense"] = round(s_sp / de["stored_breakdown"]["s_vals"], 4)
+    out["peak_ratio_sparse_over_dense"] = round(sp["peak_bytes"] / de["peak_bytes"], 4)
+    out["config"] = {"workload": name, "T": T, "d": d, "d_ff": F, "r": r}
+    return out
+
+
 def cpu_baseline(cfg: dict, sample_tokens: int) -> dict:
     import numpy as np
     from threadpoolctl import threadpool_info
@@ -122,6 +197,8 @@ def main() -> int:
     ap.add_argument("--workload", default="llama1b")
     ap.add_argument("--cpu-sample", type=int, default=16384, help="tokens for the CPU oracle baseline (0: skip)")
     ap.add_argument("--no-sparsify", action="store_true", help="skip the standalone sparsify measurement")
+    ap.add_argument("--no-large-batch", action="store_true",
+                    help="skip the T = 262144 compressed-vs-dense activation comparison")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (known traffic) for HBM counter calibration")
     args = ap.parse_args()
@@ -256,6 +333,11 @@ def main() -> int:
         result["sparsify"] = {"shape": [M, N], "avg_us": round(avg_s * 1e6, 2), "alg_bytes": alg_bytes,
                               "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                               "frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+    if not args.no_large_batch and args.workload == "llama1b":
+        print("[bench] large batch (T = 262144): compressed vs dense activations", file=sys.stderr, flush=True)
+        torch.cuda.empty_cache()
+        result["large_batch"] = large_batch_compare(steps=5, warmup=2)
 
     if args.copy_calibration:
         # a plain copy of known size: reads 1 GiB and writes 1 GiB per launch

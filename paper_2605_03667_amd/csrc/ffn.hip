@@ -100,10 +100,10 @@ using CfgNT = GemmCfg<256, BN, 4, 2, OP_K, OP_K, EPI, M_FAST, 2>;
 // 2:4 sparse A (smfmac) times K-contiguous B: 256 x 128 tiles, 2 x 4 waves.
 using CfgSP = GemmCfg<256, 128, 2, 4, OP_SP, OP_K, EPI_BF16, false, 2>;
 // Contraction over tokens (K = T): both operands stored [T x rows].
-// The dense form runs 4 x 2 waves; the 2:4 form (expanded on the way to LDS)
-// keeps 2 x 2 waves: at 8 waves its staging registers spill (measured slower).
+// Both operands are K-major: the dense ones go to LDS by DMA, the 2:4 one is
+// expanded in registers; fragments are read with the transposing LDS read.
 template <int AMODE>
-using CfgTT = GemmCfg<256, 256, (AMODE == OP_TSP ? 2 : 4), 2, AMODE, OP_T, EPI_F32, false>;
+using CfgTT = GemmCfg<256, 256, 4, 2, AMODE, OP_T, EPI_F32, false>;
 
 template <class Cfg>
 hipError_t launch(const char* tag, GemmArgs g, int splits, hipStream_t st) {

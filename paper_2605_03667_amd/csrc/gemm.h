@@ -9,27 +9,27 @@
 // as 16-byte chunks, XOR-swizzled (see swz) so that reads and writes of one
 // chunk position across 8 rows hit 8 different bank groups.
 //
-// Staging.  When both operands are K-contiguous in memory (OP_K / OP_SP) the
-// tiles go straight from global memory to LDS with global_load_lds_dwordx4
-// (no registers on the way), through STAGES LDS buffers: the loads of step
-// s + STAGES - 1 are issued while step s computes, and each wave waits only
-// for its own loads of step s (an exact vmcnt) before a plain s_barrier.
-// Lanes whose chunk lies outside the matrix load from a zero block.
-// Otherwise (a transposed operand) the next step's loads go to registers
-// before the current step's MFMAs and are written, transposed, to the other
-// of two LDS buffers after them.  Either way there is one barrier per step.
+// Staging.  Dense operands go straight from global memory to LDS with
+// global_load_lds_dwordx4 (no registers on the way), through STAGES LDS
+// buffers: the loads of step s + STAGES - 1 are issued while step s computes,
+// and each wave waits only for its own loads of step s (an exact vmcnt)
+// before a plain s_barrier.  Lanes whose chunk lies outside the matrix load
+// from a zero block.  K-contiguous operands land in K-contiguous LDS rows;
+// K-major operands ([K x rows] in memory) land K-major and their MFMA
+// fragments are read with the transposing ds_read_b64_tr_b16.  The 2:4
+// operand read along its rows (S^T, dH^T) is expanded in registers and
+// written K-major after the current step's MFMAs.  One barrier per step.
 //
 // Operand modes:
 //   OP_K    operand stored [rows x K] row-major (K contiguous): 16-byte copies.
-//   OP_T    operand stored [K x rows] (rows contiguous): each thread loads an
-//           8x8 block (8 K-rows x 8 consecutive row elements), transposes it in
-//           registers and writes 8 K-contiguous chunks.
+//   OP_T    operand stored [K x rows] (rows contiguous): DMA to a K-major LDS
+//           tile, fragments by transposing LDS reads.
 //   OP_SP   (A only) 2:4 compressed along K: kept values [rows x K/2] plus
 //           metadata [rows x K/8]; consumed by v_smfmac_f32_32x32x32_bf16.
 //   OP_TSP  (A only) 2:4 compressed along the row dimension of a [K x rows]
 //           matrix (S^T or dH^T read from the compressed activation): each
-//           thread expands 8x8 blocks from kept values + metadata to dense,
-//           transposes and writes K-contiguous chunks.
+//           thread expands 16 features of one contraction row from kept values
+//           + metadata into the K-major LDS tile.
 //
 // MFMA layouts (pinned on gfx950 by a probe against a CPU product):
 //   v_mfma_f32_32x32x16_bf16: lane l holds A[row l%32][k 8(l/32)..+8] and
@@ -104,7 +104,13 @@ struct GemmCfg {
   static constexpr int AMODE = AMODE_, BMODE = BMODE_, EPI = EPI_;
   static constexpr bool M_FAST = M_FAST_;   // consecutive tiles walk M (true) or N (false)
   static constexpr bool SPARSE = AMODE_ == OP_SP;
-  static constexpr bool DIRECT = (AMODE_ == OP_K || AMODE_ == OP_SP) && BMODE_ == OP_K;
+  // K-major operands ([K x rows] in memory) are staged K-major in LDS and read
+  // with the transposing ds_read_b64_tr_b16.
+  static constexpr bool A_KM = AMODE_ == OP_T || AMODE_ == OP_TSP;
+  static constexpr bool B_KM = BMODE_ == OP_T;
+  // DIRECT: every operand goes global -> LDS by DMA; otherwise (the 2:4
+  // K-major operand, expanded in registers) A is register-staged.
+  static constexpr bool DIRECT = AMODE_ != OP_TSP;
   static constexpr int STAGES = STAGES_;
   static constexpr int BK = SPARSE ? 128 : 64;         // dense contraction per step
   static constexpr int A_ROWB = 128;                     // bytes per LDS row of A (64 values)
@@ -118,6 +124,7 @@ struct GemmCfg {
   static_assert(NW == 4 || NW == 8, "4 or 8 waves");
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be a multiple of 32");
   static_assert(DIRECT || STAGES_ == 2, "register staging uses two LDS buffers");
+  static_assert(!(A_KM || B_KM) || !SPARSE, "2:4 along K with a K-major partner is not used");
   static_assert(STAGES_ == 2 || STAGES_ == 3, "2 or 3 stages");
   static_assert(STAGES_ * STAGE <= 160 * 1024, "LDS");
 };
@@ -127,24 +134,6 @@ struct GemmCfg {
 // the chunk with (row ^ row/8) & 7 spreads both patterns over 8 different
 // 16-byte bank groups.
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row ^ (row >> 3)) & 7); }
-
-// ---- transposes of 8x8 bf16 blocks held as 8 rows of uint4 ----------------
-// in[i] holds row i (8 consecutive elements); out[j] receives column j (the 8
-// rows' element j), so out[j] is a K-contiguous chunk when rows are K.
-__device__ __forceinline__ void transpose8x8(const uint4 (&in)[8], uint4 (&out)[8]) {
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    uint32_t w[4];
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const uint32_t* a = (const uint32_t*)&in[2 * p];
-      const uint32_t* b = (const uint32_t*)&in[2 * p + 1];
-      const uint32_t x = a[j >> 1], y = b[j >> 1];
-      w[p] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
-    }
-    out[j] = make_uint4(w[0], w[1], w[2], w[3]);
-  }
-}
 
 // Expand 2 groups (4 kept values in 8 bytes + 2 codes in one byte) to 8 dense
 // bf16 values packed as a uint4.
@@ -246,89 +235,104 @@ struct DmaMeta {
   }
 };
 
-// ---- register staging of transposed operands --------------------------------
-// Registers that carry one K step (64) of a [K x ROWS] operand from global
-// memory to LDS: each thread owns blocks of KR K-rows x 8 consecutive row
-// elements (KR = 8 for 256 threads, 4 for 512), transposed in registers on
-// the way to K-contiguous LDS rows (a block of 8 K-rows fills one 16-byte
-// chunk, a block of 4 K-rows one half chunk).
-template <int ROWS, int MODE, int NT>
-struct Stager {
-  static constexpr int ROWB = 128;
-  static constexpr int KR = NT >= 512 ? 4 : 8;
-  static constexpr int NB = (64 / KR) * (ROWS / 8) / NT;
-  static_assert(MODE == OP_T || MODE == OP_TSP, "transposed operands only");
-  static_assert(((64 / KR) * (ROWS / 8)) % NT == 0 && NB >= 1, "blocks per thread");
-  uint4 r[KR * NB];
+// ---- K-major tiles ----------------------------------------------------------
+// A K-major operand (stored [K x rows], rows contiguous) is staged as it is:
+// LDS row k (one per contraction index of the step, 64 of them) holds the
+// tile's ROWS elements, in 32-byte chunks of 16 elements; chunk c of row k
+// sits at chunk position c ^ (k & 3).
+//
+// ds_read_b64_tr_b16 (gfx950, pinned by a probe): within each group of 16
+// lanes, lane j reads 4 consecutive 16-bit elements; lane i of the group then
+// receives element i % 4 of lane 4q + i/4's read, for q = 0..3.  When lane j
+// reads row k0 + j/4 at columns c0 + 4 (j % 4), lane i therefore receives
+// column c0 + i of rows k0..k0+3: one MFMA fragment half.  The 16 lanes touch
+// rows k0..k0+3 at one logical chunk, which the swizzle spreads over four
+// bank groups.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 
-  // Global loads of the step starting at contraction index k0 (row0: first
-  // tile row; rows_valid: rows that exist; k_valid: contraction rows that exist).
-  __device__ __forceinline__ void load(const uint16_t* __restrict__ p, int64_t ld, const uint8_t* __restrict__ pm,
-                                       int64_t ldm, int64_t row0, int64_t rows_valid, int64_t k0,
-                                       int64_t k_valid, int tid) {
-    // block b -> (kb, rb) with rb fastest so a wave's lanes read consecutive
-    // pieces of the same K-row
+__device__ __forceinline__ int km_swz(int k, int chunk) { return chunk ^ (k & 3); }
+
+// Fragment of a v_mfma_f32_32x32x16_bf16 operand from a K-major LDS tile:
+// lane l gets columns col0 + l % 32, contraction indices 16 kk + 8 (l / 32) + 0..7.
+template <int ROWS>
+__device__ __forceinline__ bf16x8 frag_km(const char* base, int kk, int col0, int lane) {
+  constexpr int ROWB = ROWS * 2;
+  const int grp = lane >> 4, j = lane & 15;
+  const int k = kk * 16 + 8 * (grp >> 1) + (j >> 2);
+  const int col = col0 + 16 * (grp & 1) + 4 * (j & 3);
+  const int c = col >> 4, w = (col & 15) * 2;
+  const char* p0 = base + k * ROWB + (km_swz(k, c) << 5) + w;
+  const char* p1 = base + (k + 4) * ROWB + (km_swz(k + 4, c) << 5) + w;
+  const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p0);
+  const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p1);
+  const s16x4 lo = a, hi = b;
+  typedef short s16x8 __attribute__((ext_vector_type(8)));
+  const s16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// A dense K-major tile [64 x ROWS] copied by DMA: 1 KB blocks, PER_WAVE per
+// wave; lane i fills the block's 16-byte unit i, i.e. physical unit (i mod
+// units per row) of row (block rows + i / units per row), and fetches the
+// global 8 elements that the swizzle maps there.
+template <int ROWS, int NW>
+struct DmaTileKM {
+  static constexpr int ROWB = ROWS * 2;
+  static constexpr int BLOCKS = 64 * ROWB / 1024;
+  static constexpr int PER_WAVE = BLOCKS / NW;
+  static_assert(BLOCKS % NW == 0 && ROWB <= 1024, "blocks per wave");
+  template <int J0, int J1>
+  __device__ __forceinline__ static void issue(const uint16_t* __restrict__ p, int64_t ld, int64_t col0,
+                                               int64_t cols_valid, int64_t k0, int64_t k_valid, uint32_t lds,
+                                               int wave, int lane) {
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const int u = b * NT + tid;
-      const int rb = u % (ROWS / 8), kb = u / (ROWS / 8);
-      const int64_t grow = row0 + rb * 8;
-      const bool rok = grow < rows_valid;
+    for (int j = J0; j < J1; ++j) {
+      const int blk = wave * PER_WAVE + j;
+      const int off = blk * 1024 + lane * 16;
+      const int k = off / ROWB, pu = (off % ROWB) / 16;
+      const int col = km_swz(k, pu >> 1) * 16 + (pu & 1) * 8;
+      const int64_t gk = k0 + k, gc = col0 + col;
+      const void* src = (gk < k_valid && gc < cols_valid) ? (const void*)(p + gk * ld + gc) : (const void*)g_dma_zero;
+      dma_b128(src, __builtin_amdgcn_readfirstlane(lds + blk * 1024));
+    }
+  }
+};
+
+// A 2:4 K-major tile: rows of kept values [K x cols/2] + metadata [K x cols/8]
+// (the compressed activation read along tokens).  Each thread loads the kept
+// values (16 bytes) and codes (2 bytes) of 16 consecutive features of one
+// contraction row, and after the current step's MFMAs writes them expanded
+// (32 bytes) into the K-major LDS tile; no transpose is needed.
+template <int ROWS, int NT>
+struct StagerKMSP {
+  static constexpr int ROWB = ROWS * 2;
+  static constexpr int CHUNKS = ROWS / 16;
+  static constexpr int NU = 64 * CHUNKS / NT;
+  static_assert((64 * CHUNKS) % NT == 0, "units per thread");
+  uint4 v[NU];
+  uint32_t m[NU];
+  __device__ __forceinline__ void load(const uint16_t* __restrict__ pv, int64_t ldv, const uint8_t* __restrict__ pm,
+                                       int64_t ldm, int64_t col0, int64_t cols_valid, int64_t k0, int64_t k_valid,
+                                       int tid) {
 #pragma unroll
-      for (int i = 0; i < KR; ++i) {
-        const int64_t gk = k0 + kb * KR + i;
-        uint4 v = make_uint4(0u, 0u, 0u, 0u);
-        if (rok && gk < k_valid) {
-          if constexpr (MODE == OP_T) {
-            v = *(const uint4*)(p + gk * ld + grow);
-          } else {
-            // raw kept values + codes; expanded in store(), after the MFMAs,
-            // so the loads stay in flight during the current step
-            const uint2 kept = *(const uint2*)(p + gk * ld + grow / 2);
-            v = make_uint4(kept.x, kept.y, pm[gk * ldm + grow / 8], 0u);
-          }
-        }
-        r[KR * b + i] = v;
+    for (int u = 0; u < NU; ++u) {
+      const int q = u * NT + tid, k = q / CHUNKS, c = q % CHUNKS;
+      const int64_t gk = k0 + k, f = col0 + 16 * c;
+      v[u] = make_uint4(0u, 0u, 0u, 0u);
+      m[u] = 0u;
+      if (gk < k_valid && f < cols_valid) {
+        v[u] = *(const uint4*)(pv + gk * ldv + f / 2);
+        m[u] = *(const uint16_t*)(pm + gk * ldm + f / 8);
       }
     }
   }
-
   __device__ __forceinline__ void store(char* lds, int tid) const {
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const int u = b * NT + tid;
-      const int rb = u % (ROWS / 8), kb = u / (ROWS / 8);
-      uint4 in[8];
-#pragma unroll
-      for (int i = 0; i < KR; ++i) {
-        if constexpr (MODE == OP_TSP)
-          in[i] = expand2(make_uint2(r[KR * b + i].x, r[KR * b + i].y), r[KR * b + i].z);
-        else
-          in[i] = r[KR * b + i];
-      }
-      if constexpr (KR == 8) {
-        uint4 out[8];
-        transpose8x8(in, out);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int row = rb * 8 + j;
-          *(uint4*)(lds + row * ROWB + swz(row, kb) * 16) = out[j];
-        }
-      } else {
-        // 4 K-rows: element j of the 4 rows -> half chunk (kb & 1) of chunk kb/2
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          uint32_t w[2];
-#pragma unroll
-          for (int q = 0; q < 2; ++q) {
-            const uint32_t x = ((const uint32_t*)&in[2 * q])[j >> 1];
-            const uint32_t y = ((const uint32_t*)&in[2 * q + 1])[j >> 1];
-            w[q] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
-          }
-          const int row = rb * 8 + j;
-          *(uint2*)(lds + row * ROWB + swz(row, kb >> 1) * 16 + (kb & 1) * 8) = make_uint2(w[0], w[1]);
-        }
-      }
+    for (int u = 0; u < NU; ++u) {
+      const int q = u * NT + tid, k = q / CHUNKS, c = q % CHUNKS;
+      char* dst = lds + k * ROWB + (km_swz(k, c) << 5);
+      *(uint4*)dst = expand2(make_uint2(v[u].x, v[u].y), m[u] & 0xFFu);
+      *(uint4*)(dst + 16) = expand2(make_uint2(v[u].z, v[u].w), m[u] >> 8);
     }
   }
 };
@@ -386,13 +390,21 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       auto read = [&](int kk, int slot) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
-          const int row = wm * TM + i * 32 + lrow;
-          af[slot][i] = *(const bf16x8*)(lA + row * 128 + swz(row, 2 * kk + lhalf) * 16);
+          if constexpr (Cfg::A_KM) {
+            af[slot][i] = frag_km<BM>(lA, kk, wm * TM + i * 32, lane);
+          } else {
+            const int row = wm * TM + i * 32 + lrow;
+            af[slot][i] = *(const bf16x8*)(lA + row * 128 + swz(row, 2 * kk + lhalf) * 16);
+          }
         }
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-          const int row = wn * TN + j * 32 + lrow;
-          bfr[slot][j] = *(const bf16x8*)(lB + row * 128 + swz(row, 2 * kk + lhalf) * 16);
+          if constexpr (Cfg::B_KM) {
+            bfr[slot][j] = frag_km<BN>(lB, kk, wn * TN + j * 32, lane);
+          } else {
+            const int row = wn * TN + j * 32 + lrow;
+            bfr[slot][j] = *(const bf16x8*)(lB + row * 128 + swz(row, 2 * kk + lhalf) * 16);
+          }
         }
       };
       if constexpr (Cfg::PIPE) read(0, 0);
@@ -456,8 +468,8 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
   };
 
   if constexpr (Cfg::DIRECT) {
-    using TA = DmaTile<BM, Cfg::A_ROWB, SPARSE, NW>;
-    using TB = DmaTile<BN, Cfg::B_ROWB, false, NW>;
+    using TA = std::conditional_t<Cfg::A_KM, DmaTileKM<BM, NW>, DmaTile<BM, Cfg::A_ROWB, SPARSE, NW>>;
+    using TB = std::conditional_t<Cfg::B_KM, DmaTileKM<BN, NW>, DmaTile<BN, Cfg::B_ROWB, false, NW>>;
     using TMeta = DmaMeta<BM, (SPARSE ? NW : 1)>;
     constexpr int LA = TA::PER_WAVE, LB = TB::PER_WAVE, LM = SPARSE ? TMeta::PER_WAVE : 0;
     constexpr int LOADS = LA + LB + LM;   // DMA instructions per wave per step
@@ -520,39 +532,33 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       });
     }
   } else {
-    Stager<BM, Cfg::AMODE, NT> sa;
-    Stager<BN, Cfg::BMODE, NT> sb;
-    auto load_step = [&](int64_t k0) __attribute__((always_inline)) {
-      sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, k0, g.ka_valid, tid);
-      sb.load(g.B, g.ldb, nullptr, 0, n0, g.N, k0, g.kb_valid, tid);
-    };
-    auto store_step = [&](int buf) __attribute__((always_inline)) {
-      char* base = smem + buf * Cfg::STAGE;
-      sa.store(base, tid);
-      sb.store(base + Cfg::A_BYTES, tid);
+    // A: the 2:4 K-major operand, expanded in registers; B: DMA.  The next
+    // step's A loads and B DMA are issued before the current step's MFMAs; A
+    // is written to LDS after them; one barrier per step.
+    StagerKMSP<BM, NT> sa;
+    using TB = std::conditional_t<Cfg::B_KM, DmaTileKM<BN, NW>, DmaTile<BN, Cfg::B_ROWB, false, NW>>;
+    const uint32_t smem_lds = lds_u32(smem);
+    auto issue_b = [&](int step) __attribute__((always_inline)) {
+      const int64_t k0 = kbeg + (int64_t)step * BK;
+      const uint32_t base = smem_lds + (uint32_t)((step & 1) * Cfg::STAGE) + Cfg::A_BYTES;
+      TB::template issue<0, TB::PER_WAVE>(g.B, g.ldb, n0, g.N, k0, g.kb_valid, base, wave, lane);
     };
     if (nsteps > 0) {
-      load_step(kbeg);
-      store_step(0);
+      sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, kbeg, g.ka_valid, tid);
+      issue_b(0);
+      sa.store(smem, tid);
       __syncthreads();
     }
     for (int s = 0; s < nsteps; ++s) {
       const int buf = s & 1;
       const bool more = s + 1 < nsteps;
-      if (more) load_step(kbeg + (int64_t)(s + 1) * BK);
-      if constexpr (Cfg::AMODE == OP_T) {
-        // the next step's transposing LDS writes go in before the last
-        // sub-step's MFMAs, so they overlap the matrix cores' work
-        compute(smem + buf * Cfg::STAGE, [&](int kk) __attribute__((always_inline)) {
-          if (kk == 3 && more) store_step(buf ^ 1);
-        });
-      } else {
-        // the 2:4 expansion needs more registers than are free during the
-        // MFMAs (spills), so it runs after them
-        compute(smem + buf * Cfg::STAGE, [](int) {});
-        if (more) store_step(buf ^ 1);
+      if (more) {
+        sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, kbeg + (int64_t)(s + 1) * BK, g.ka_valid, tid);
+        issue_b(s + 1);
       }
-      __syncthreads();
+      compute(smem + buf * Cfg::STAGE, [](int) {});
+      if (more) sa.store(smem + (buf ^ 1) * Cfg::STAGE, tid);
+      __syncthreads();   // A's LDS writes and B's DMA of step s+1 are complete
     }
   }
 
