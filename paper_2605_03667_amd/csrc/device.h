@@ -25,6 +25,16 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float x) {
   return u >> 16;
 }
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Two floats -> two bf16 (the hardware conversion, round to nearest even)
+// packed as lo | hi << 16: one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t bf16x2_rne(float lo, float hi) {
+  const f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint32_t b) {
   return __builtin_bit_cast(float, b << 16);
 }
@@ -36,6 +46,65 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t b) {
 // ranking key of Algorithm 1 on s.
 __device__ __forceinline__ uint32_t relu_bits(uint32_t b) {
   return ((int32_t)(int16_t)b > 0 && b <= 0x7F80u) ? b : 0u;
+}
+
+// relu on two packed bf16 (lo | hi << 16), with the same result as relu_bits
+// on each half: negative values, -0 and NaN become 0.  After the signed
+// max with 0, adding 0x7F moves exactly the NaN patterns (0x7F81..0x7FFF)
+// past 0x7FFF; the second max sends them to 0x7F, and subtracting 0x7F
+// restores every other value.  Four packed 16-bit operations.
+__device__ __forceinline__ uint32_t relu_bits2(uint32_t p) {
+  typedef short s16x2 __attribute__((ext_vector_type(2)));
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  const s16x2 zero = {0, 0}, c7f = {0x7F, 0x7F};
+  const u16x2 u7f = {0x7F, 0x7F};
+  s16x2 v = __builtin_elementwise_max(__builtin_bit_cast(s16x2, p), zero);
+  v = __builtin_bit_cast(s16x2, __builtin_bit_cast(u16x2, v) + u7f);
+  v = __builtin_elementwise_max(v, c7f);
+  return __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, v) - u7f);
+}
+
+// Top-2 of a group of four from two packed relu'd pairs (p01 = r0 | r1 << 16,
+// p23 = r2 | r3 << 16), as Algorithm 1 ranks them: by value, ties to the lower
+// index.  Each element becomes the unique key r << 2 | (3 - i), so that a
+// plain maximum implements the tie rule.  With a, b the larger and smaller
+// key of elements 0, 1 and c, d those of 2, 3, the largest key is max(a, c)
+// and the second largest max(min(a, c), max(b, d)).  Rotating the index bits
+// to the top orders the two kept elements
+// by index.
+struct Top2 {
+  uint32_t first, second;   // r | (3 - i) << 30 of the kept elements, i0 < i1
+};
+__device__ __forceinline__ Top2 top2_keys(uint32_t p01, uint32_t p23) {
+  const uint32_t k0 = ((p01 & 0xFFFFu) << 2) | 3u;
+  const uint32_t k1 = ((p01 >> 14) & 0x3FFFCu) | 2u;
+  const uint32_t k2 = ((p23 & 0xFFFFu) << 2) | 1u;
+  const uint32_t k3 = (p23 >> 14) & 0x3FFFCu;
+  const uint32_t a = k0 > k1 ? k0 : k1, b = k0 > k1 ? k1 : k0;
+  const uint32_t c = k2 > k3 ? k2 : k3, d = k2 > k3 ? k3 : k2;
+  const uint32_t t1 = a > c ? a : c;
+  const uint32_t e = b > d ? b : d, f = a > c ? c : a;
+  const uint32_t t2 = e > f ? e : f;
+  const uint32_t r1 = __builtin_amdgcn_alignbit(t1, t1, 2), r2 = __builtin_amdgcn_alignbit(t2, t2, 2);
+  Top2 t;
+  t.first = r1 > r2 ? r1 : r2;
+  t.second = r1 > r2 ? r2 : r1;
+  return t;
+}
+// Code i0 | i1 << 2 of a Top2 result.
+__device__ __forceinline__ uint32_t top2_code_of(const Top2& t) {
+  return 15u - ((t.first >> 30) | ((t.second >> 30) << 2));
+}
+
+// Square root rounded to bf16 for a non-negative bf16 value s given as fp32.
+// The raw v_sqrt_f32 result rounds to the same bf16 as the correctly rounded
+// square root for every such s with a normal exponent (checked over all bf16
+// inputs on gfx950); subnormal inputs, which v_sqrt_f32 flushes, are scaled
+// by 2^64 first and the root by 2^-32 after (both exact).  The caller rounds.
+__device__ __forceinline__ float sqrt_for_bf16(float s) {
+  const bool tiny = s < 0x1p-126f;
+  const float r = __builtin_amdgcn_sqrtf(tiny ? s * 0x1p64f : s);
+  return tiny ? r * 0x1p-32f : r;
 }
 
 // Stable top-2 of four keys (ties go to the lower index).  Returns the 4-bit

@@ -104,6 +104,10 @@ struct GemmCfg {
   static constexpr int AMODE = AMODE_, BMODE = BMODE_, EPI = EPI_;
   static constexpr bool M_FAST = M_FAST_;   // consecutive tiles walk M (true) or N (false)
   static constexpr bool SPARSE = AMODE_ == OP_SP;
+  // SWAP: the MFMAs take B's fragment as their first operand, so that each
+  // lane accumulates runs of consecutive C columns (plain bf16 / fp32 output,
+  // written with 16-byte stores).  The 2:4 operand must stay first.
+  static constexpr bool SWAP = !SPARSE && (EPI_ == EPI_BF16 || EPI_ == EPI_F32);
   // K-major operands ([K x rows] in memory) are staged K-major in LDS and read
   // with the transposing ds_read_b64_tr_b16.
   static constexpr bool A_KM = AMODE_ == OP_T || AMODE_ == OP_TSP;
@@ -165,11 +169,33 @@ __device__ __forceinline__ uint32_t lds_u32(const void* p) {
 // lds_wave_base + 16 i (4 i).  The base must be wave-uniform (it goes to M0).
 // Issued through inline asm so that the compiler does not guard every later
 // LDS access with a full vmcnt(0); the kernel waits with exact counts itself.
+// M0 is written here and read only by the DMA that follows; the generated
+// code of these kernels uses M0 nowhere else (checked in the ISA).
 __device__ __forceinline__ void dma_b128(const void* g, uint32_t lds_wave_base) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_wave_base) : "memory", "m0");
 }
 __device__ __forceinline__ void dma_b32(const void* g, uint32_t lds_wave_base) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds_wave_base) : "memory", "m0");
+}
+// The same DMA addressed as a wave-uniform 64-bit base (SGPRs) plus a 32-bit
+// per-lane byte offset: no per-lane 64-bit address arithmetic.  The base is
+// uniform by construction; readfirstlane states it to the compiler (and is
+// free when it already sits in SGPRs).
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+  const uint64_t u = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  return (const void*)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ void dma_b128_s(const void* sbase, uint32_t voff, uint32_t lds_wave_base) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(uniform_ptr(sbase)),
+               "s"(lds_wave_base)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma_b32_s(const void* sbase, uint32_t voff, uint32_t lds_wave_base) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(voff), "s"(uniform_ptr(sbase)),
+               "s"(lds_wave_base)
+               : "memory", "m0");
 }
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -208,6 +234,24 @@ struct DmaTile {
       dma_b128(src, __builtin_amdgcn_readfirstlane(lds + blk * 1024));
     }
   }
+  // Unchecked path, for a tile and step that lie inside the matrix: the byte
+  // offset of load j's chunk from the tile's first row at the step's first
+  // contraction element (constant over the steps), and the issue from a
+  // wave-uniform base.
+  __device__ __forceinline__ static uint32_t lane_off(int j, int64_t ld, int wave, int lane) {
+    const int blk = wave * PER_WAVE + j;
+    const int off = blk * 1024 + lane * 16;
+    const int row = off / ROWB, pos = (off % ROWB) / 16;
+    return (uint32_t)row * (uint32_t)(ld * 2) + (uint32_t)swz(row, pos) * 16u;
+  }
+  __device__ __forceinline__ static const char* step_base(const uint16_t* p, int64_t ld, int64_t row0, int64_t k0) {
+    return (const char*)(p + row0 * ld + (KEPT ? k0 / 2 : k0));
+  }
+  template <int J0, int J1>
+  __device__ __forceinline__ static void issue_fast(const char* sbase, const uint32_t* voff, uint32_t lds, int wave) {
+#pragma unroll
+    for (int j = J0; j < J1; ++j) dma_b128_s(sbase, voff[j], lds + (wave * PER_WAVE + j) * 1024);
+  }
 };
 
 // Metadata of a 2:4 tile: ROWS rows x 16 bytes (128 dense K), dword DMA
@@ -232,6 +276,19 @@ struct DmaMeta {
                             : (const void*)g_dma_zero;
       dma_b32(src, __builtin_amdgcn_readfirstlane(lds + blk * 256));
     }
+  }
+  __device__ __forceinline__ static uint32_t lane_off(int j, int64_t ldm, int wave, int lane) {
+    const int blk = wave * PER_WAVE + j;
+    const int off = blk * 256 + lane * 4;
+    return (uint32_t)(off / 16) * (uint32_t)ldm + (uint32_t)(off % 16);
+  }
+  __device__ __forceinline__ static const char* step_base(const uint8_t* pm, int64_t ldm, int64_t row0, int64_t k0) {
+    return (const char*)(pm + row0 * ldm + k0 / 8);
+  }
+  template <int J0, int J1>
+  __device__ __forceinline__ static void issue_fast(const char* sbase, const uint32_t* voff, uint32_t lds, int wave) {
+#pragma unroll
+    for (int j = J0; j < J1; ++j) dma_b32_s(sbase, voff[j], lds + (wave * PER_WAVE + j) * 256);
   }
 };
 
@@ -296,6 +353,21 @@ struct DmaTileKM {
       dma_b128(src, __builtin_amdgcn_readfirstlane(lds + blk * 1024));
     }
   }
+  __device__ __forceinline__ static uint32_t lane_off(int j, int64_t ld, int wave, int lane) {
+    const int blk = wave * PER_WAVE + j;
+    const int off = blk * 1024 + lane * 16;
+    const int k = off / ROWB, pu = (off % ROWB) / 16;
+    const int col = km_swz(k, pu >> 1) * 16 + (pu & 1) * 8;
+    return (uint32_t)k * (uint32_t)(ld * 2) + (uint32_t)col * 2u;
+  }
+  __device__ __forceinline__ static const char* step_base(const uint16_t* p, int64_t ld, int64_t col0, int64_t k0) {
+    return (const char*)(p + k0 * ld + col0);
+  }
+  template <int J0, int J1>
+  __device__ __forceinline__ static void issue_fast(const char* sbase, const uint32_t* voff, uint32_t lds, int wave) {
+#pragma unroll
+    for (int j = J0; j < J1; ++j) dma_b128_s(sbase, voff[j], lds + (wave * PER_WAVE + j) * 1024);
+  }
 };
 
 // A 2:4 K-major tile: rows of kept values [K x cols/2] + metadata [K x cols/8]
@@ -356,7 +428,8 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
   __shared__ __attribute__((aligned(1024))) char smem[STAGES * Cfg::STAGE];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform, so derived LDS bases are scalar
   const int wm = wave / Cfg::WAVES_N, wn = wave % Cfg::WAVES_N;
   const int ntiles = g.tiles_m * g.tiles_n;
   const int tile = xcd_remap(blockIdx.x, ntiles);
@@ -421,7 +494,8 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         for (int i = 0; i < FM; ++i)
 #pragma unroll
           for (int j = 0; j < FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
+            acc[i][j] = Cfg::SWAP ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0)
+                                  : __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
       }
     } else {
       uint4 meta[FM];
@@ -474,9 +548,46 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     constexpr int LA = TA::PER_WAVE, LB = TB::PER_WAVE, LM = SPARSE ? TMeta::PER_WAVE : 0;
     constexpr int LOADS = LA + LB + LM;   // DMA instructions per wave per step
     const uint32_t smem_lds = lds_u32(smem);
+    // Steps of a tile that lies inside both operands take the unchecked path:
+    // per-lane offsets computed once, a scalar base per step.
+    uint32_t offA[LA], offB[LB], offM[LM > 0 ? LM : 1];
+#pragma unroll
+    for (int j = 0; j < LA; ++j) offA[j] = TA::lane_off(j, g.lda, wave, lane);
+#pragma unroll
+    for (int j = 0; j < LB; ++j) offB[j] = TB::lane_off(j, g.ldb, wave, lane);
+    if constexpr (SPARSE) {
+#pragma unroll
+      for (int j = 0; j < LM; ++j) offM[j] = TMeta::lane_off(j, g.ldam, wave, lane);
+    }
+    // Steps [0, steps_in) of a tile inside both operands read no element
+    // outside them: their loads skip the bounds checks.
+    int steps_in = 0;
+    if (m0 + BM <= g.m_valid && n0 + BN <= g.N) {
+      const int64_t k_in = (g.ka_valid < g.kb_valid ? g.ka_valid : g.kb_valid) - kbeg;
+      steps_in = k_in <= 0 ? 0 : (int)(k_in / BK < nsteps ? k_in / BK : nsteps);
+    }
+    steps_in = __builtin_amdgcn_readfirstlane(steps_in);
     // Issue the loads of `step`, part q of 4 (A first half, A second half +
-    // metadata, B first half, B second half).
-    auto issue_part = [&](int step, auto q) __attribute__((always_inline)) {
+    // metadata, B first half, B second half), unchecked or checked.
+    auto fast_part = [&](int step, auto q) __attribute__((always_inline)) {
+      const int64_t k0 = kbeg + (int64_t)step * BK;
+      const uint32_t base = smem_lds + (uint32_t)((step % STAGES) * Cfg::STAGE);
+      constexpr int Q = decltype(q)::value;
+      if constexpr (Q == 0) {
+        TA::template issue_fast<0, LA / 2>(TA::step_base(g.A, g.lda, m0, k0), offA, base, wave);
+      } else if constexpr (Q == 1) {
+        TA::template issue_fast<LA / 2, LA>(TA::step_base(g.A, g.lda, m0, k0), offA, base, wave);
+        if constexpr (SPARSE)
+          TMeta::template issue_fast<0, LM>(TMeta::step_base(g.Am, g.ldam, m0, k0), offM, base + Cfg::A_BYTES, wave);
+      } else if constexpr (Q == 2) {
+        TB::template issue_fast<0, LB / 2>(TB::step_base(g.B, g.ldb, n0, k0), offB, base + Cfg::A_BYTES + Cfg::AM_BYTES,
+                                           wave);
+      } else {
+        TB::template issue_fast<LB / 2, LB>(TB::step_base(g.B, g.ldb, n0, k0), offB,
+                                            base + Cfg::A_BYTES + Cfg::AM_BYTES, wave);
+      }
+    };
+    auto slow_part = [&](int step, auto q) __attribute__((always_inline)) {
       const int64_t k0 = kbeg + (int64_t)step * BK;
       const uint32_t base = smem_lds + (uint32_t)((step % STAGES) * Cfg::STAGE);
       constexpr int Q = decltype(q)::value;
@@ -494,11 +605,24 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
                                        wave, lane);
       }
     };
+    auto issue_part = [&](int step, auto q) __attribute__((always_inline)) {
+      if (step < steps_in)
+        fast_part(step, q);
+      else
+        slow_part(step, q);
+    };
     auto issue_all = [&](int step) __attribute__((always_inline)) {
-      issue_part(step, std::integral_constant<int, 0>{});
-      issue_part(step, std::integral_constant<int, 1>{});
-      issue_part(step, std::integral_constant<int, 2>{});
-      issue_part(step, std::integral_constant<int, 3>{});
+      if (step < steps_in) {
+        fast_part(step, std::integral_constant<int, 0>{});
+        fast_part(step, std::integral_constant<int, 1>{});
+        fast_part(step, std::integral_constant<int, 2>{});
+        fast_part(step, std::integral_constant<int, 3>{});
+      } else {
+        slow_part(step, std::integral_constant<int, 0>{});
+        slow_part(step, std::integral_constant<int, 1>{});
+        slow_part(step, std::integral_constant<int, 2>{});
+        slow_part(step, std::integral_constant<int, 3>{});
+      }
     };
 #pragma unroll
     for (int p = 0; p < STAGES - 1; ++p)
@@ -538,10 +662,22 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     StagerKMSP<BM, NT> sa;
     using TB = std::conditional_t<Cfg::B_KM, DmaTileKM<BN, NW>, DmaTile<BN, Cfg::B_ROWB, false, NW>>;
     const uint32_t smem_lds = lds_u32(smem);
+    uint32_t offB[TB::PER_WAVE];
+#pragma unroll
+    for (int j = 0; j < TB::PER_WAVE; ++j) offB[j] = TB::lane_off(j, g.ldb, wave, lane);
+    int b_steps_in = 0;   // steps whose B loads need no bounds checks
+    if (n0 + BN <= g.N) {
+      const int64_t k_in = g.kb_valid - kbeg;
+      b_steps_in = k_in <= 0 ? 0 : (int)(k_in / BK < nsteps ? k_in / BK : nsteps);
+    }
+    b_steps_in = __builtin_amdgcn_readfirstlane(b_steps_in);
     auto issue_b = [&](int step) __attribute__((always_inline)) {
       const int64_t k0 = kbeg + (int64_t)step * BK;
       const uint32_t base = smem_lds + (uint32_t)((step & 1) * Cfg::STAGE) + Cfg::A_BYTES;
-      TB::template issue<0, TB::PER_WAVE>(g.B, g.ldb, n0, g.N, k0, g.kb_valid, base, wave, lane);
+      if (step < b_steps_in)
+        TB::template issue_fast<0, TB::PER_WAVE>(TB::step_base(g.B, g.ldb, n0, k0), offB, base, wave);
+      else
+        TB::template issue<0, TB::PER_WAVE>(g.B, g.ldb, n0, g.N, k0, g.kb_valid, base, wave, lane);
     };
     if (nsteps > 0) {
       sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, kbeg, g.ka_valid, tid);
@@ -563,7 +699,55 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
   }
 
   // ---------------------------------------------------------------- epilogues
-  if constexpr (Cfg::EPI == EPI_BF16 || Cfg::EPI == EPI_F32) {
+  if constexpr (Cfg::SWAP) {
+    // Accumulator 4b+q of lane l is C[row l%32][col 8b + 4h + q] of its 32x32
+    // block (h = l / 32).  N is a multiple of 8, so each 8-column (bf16) or
+    // 4-column (fp32) piece is wholly inside or outside the matrix.
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int64_t row = m0 + wm * TM + i * 32 + lrow;
+        const int64_t colb = n0 + wn * TN + j * 32;
+        if constexpr (Cfg::EPI == EPI_BF16) {
+          // pk[b]: columns 8b+4h .. +3 as two bf16 pairs.  One permlane32 swap
+          // per dword gives lane half 0 columns 0..15 and half 1 columns 16..31.
+          uint32_t pk[4][2];
+#pragma unroll
+          for (int b = 0; b < 4; ++b)
+#pragma unroll
+            for (int e = 0; e < 2; ++e)
+              pk[b][e] = bf16x2_rne(acc[i][j][4 * b + 2 * e], acc[i][j][4 * b + 2 * e + 1]);
+          uint32_t out[2][4];
+#pragma unroll
+          for (int c = 0; c < 2; ++c)
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+              const auto sw = __builtin_amdgcn_permlane32_swap(pk[c][e], pk[c + 2][e], false, false);
+              out[c][e] = sw[0];       // half 0: columns 8c + 2e ..; half 1: 16 + 8c + 2e ..
+              out[c][2 + e] = sw[1];   // half 0: columns 8c + 4 + 2e ..; half 1: 16 + 8c + 4 + 2e ..
+            }
+          const int64_t col = colb + 16 * lhalf;
+          if (row < g.M) {
+            __bf16* dst = (__bf16*)g.C + row * g.ldc + col;
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+              if (col + 8 * c < g.N) *(uint4*)(dst + 8 * c) = make_uint4(out[c][0], out[c][1], out[c][2], out[c][3]);
+          }
+        } else {
+          float* part = (float*)g.C + (int64_t)blockIdx.y * g.M * g.N;
+          if (row < g.M) {
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+              const int64_t col = colb + 8 * b + 4 * lhalf;
+              if (col < g.N)
+                *(float4*)(part + row * g.N + col) =
+                    make_float4(acc[i][j][4 * b], acc[i][j][4 * b + 1], acc[i][j][4 * b + 2], acc[i][j][4 * b + 3]);
+            }
+          }
+        }
+      }
+  } else if constexpr (Cfg::EPI == EPI_BF16 || Cfg::EPI == EPI_F32) {
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -598,19 +782,19 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         if constexpr (Cfg::EPI == EPI_ACT_DENSE) {
 #pragma unroll
           for (int b = 0; b < 4; ++b) {
-            uint32_t v[4];
+            uint32_t v[2];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const __bf16 hb = (__bf16)acc[i][j][4 * b + q];       // h rounded to bf16 (RNE)
-              const uint32_t r = relu_bits(__builtin_bit_cast(uint16_t, hb));
+            for (int e = 0; e < 2; ++e) {
+              // h rounded to bf16 (RNE), relu'd, squared (act_square) and rounded
+              const uint32_t r = relu_bits2(bf16x2_rne(acc[i][j][4 * b + 2 * e], acc[i][j][4 * b + 2 * e + 1]));
               if (g.act_square) {
-                const float a = bf16_to_f32(r);
-                v[q] = f32_to_bf16_rne(a * a);
+                const float lo = __builtin_bit_cast(float, r << 16), hi = __builtin_bit_cast(float, r & 0xFFFF0000u);
+                v[e] = bf16x2_rne(lo * lo, hi * hi);
               } else {
-                v[q] = r;
+                v[e] = r;
               }
             }
-            mine[b] = make_uint2(v[0] | (v[1] << 16), v[2] | (v[3] << 16));
+            mine[b] = make_uint2(v[0], v[1]);
           }
         } else {
 #pragma unroll
@@ -618,35 +802,41 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             const int64_t f = f32 + 8 * b + 4 * lhalf;
             uint2 a = make_uint2(0u, 0u);
             if (t < g.N && f < g.f_valid) a = *(const uint2*)(g.act + t * g.ld_act + f);
-            const uint32_t av[4] = {a.x & 0xFFFFu, a.x >> 16, a.y & 0xFFFFu, a.y >> 16};
-            uint32_t v[4];
+            uint32_t v[2];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const float x = bf16_to_f32(av[q]);
-              const float r = g.act_square ? (float)(__bf16)__builtin_sqrtf(x) : x;
-              v[q] = __builtin_bit_cast(uint16_t, (__bf16)(acc[i][j][4 * b + q] * 2.0f * r));
+            for (int e = 0; e < 2; ++e) {
+              const uint32_t w = e ? a.y : a.x;
+              float x0 = __builtin_bit_cast(float, w << 16), x1 = __builtin_bit_cast(float, w & 0xFFFF0000u);
+              if (g.act_square) {   // r = bf16(sqrt(a)) recovers relu(h) exactly
+                const uint32_t rr = bf16x2_rne(sqrt_for_bf16(x0), sqrt_for_bf16(x1));
+                x0 = __builtin_bit_cast(float, rr << 16);
+                x1 = __builtin_bit_cast(float, rr & 0xFFFF0000u);
+              }
+              v[e] = bf16x2_rne(acc[i][j][4 * b + 2 * e] * 2.0f * x0, acc[i][j][4 * b + 2 * e + 1] * 2.0f * x1);
             }
-            mine[b] = make_uint2(v[0] | (v[1] << 16), v[2] | (v[3] << 16));
+            mine[b] = make_uint2(v[0], v[1]);
           }
         }
-        // half 0 needs the partner's blocks 0,1; half 1 the partner's 2,3
-        const uint2 give0 = lhalf ? mine[0] : mine[2];
-        const uint2 give1 = lhalf ? mine[1] : mine[3];
-        const uint2 got0 = make_uint2(__shfl_xor(give0.x, 32), __shfl_xor(give0.y, 32));
-        const uint2 got1 = make_uint2(__shfl_xor(give1.x, 32), __shfl_xor(give1.y, 32));
-        uint4 lo, hi;   // features +0..7 and +8..15 of this lane's 16
-        if (lhalf == 0) {
-          lo = make_uint4(mine[0].x, mine[0].y, got0.x, got0.y);
-          hi = make_uint4(mine[1].x, mine[1].y, got1.x, got1.y);
-        } else {
-          lo = make_uint4(got0.x, got0.y, mine[2].x, mine[2].y);
-          hi = make_uint4(got1.x, got1.y, mine[3].x, mine[3].y);
+        // Half 0 keeps features 0..15 of the block, half 1 features 16..31:
+        // swapping (block 0, block 2) and (block 1, block 3) across the halves
+        // leaves each lane two runs of 8 consecutive features.
+        uint32_t lo[4], hi[4];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const auto s0 = __builtin_amdgcn_permlane32_swap(e ? mine[0].y : mine[0].x, e ? mine[2].y : mine[2].x,
+                                                           false, false);
+          const auto s1 = __builtin_amdgcn_permlane32_swap(e ? mine[1].y : mine[1].x, e ? mine[3].y : mine[3].x,
+                                                           false, false);
+          lo[e] = s0[0];
+          lo[2 + e] = s0[1];
+          hi[e] = s1[0];
+          hi[2 + e] = s1[1];
         }
         const int64_t f = f32 + 16 * lhalf;
         if (t < g.N) {
           uint16_t* dst = (Cfg::EPI == EPI_ACT_DENSE ? g.act : g.dact) + t * g.ld_act + f;
-          if (f + 8 <= g.f_valid) *(uint4*)dst = lo;
-          if (f + 16 <= g.f_valid) *(uint4*)(dst + 8) = hi;
+          if (f + 8 <= g.f_valid) *(uint4*)dst = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+          if (f + 16 <= g.f_valid) *(uint4*)(dst + 8) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
         }
       }
   } else {
@@ -704,32 +894,26 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         const bool ok = tl < t_end && fl < f_end;
         uint32_t pair[4], codes = 0;
         if constexpr (Cfg::EPI == EPI_SPARSIFY) {
+          uint32_t codes = 0;   // code of group b at bits 8b .. 8b+3
 #pragma unroll
           for (int b = 0; b < 4; ++b) {
-            uint32_t r[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const __bf16 hb = (__bf16)acc[i][j][4 * b + q];      // h rounded to bf16 (RNE)
-              r[q] = relu_bits(__builtin_bit_cast(uint16_t, hb));
-            }
-            const uint32_t code = top2_code(r[0], r[1], r[2], r[3]);
-            const uint32_t kept = pick_pair(code, r[0], r[1], r[2], r[3]);
-            const float a = bf16_to_f32(kept & 0xFFFFu), c = bf16_to_f32(kept >> 16);
-            pair[b] = f32_to_bf16_rne(a * a) | (f32_to_bf16_rne(c * c) << 16);
-            codes |= code << (4 * b);
+            // h rounded to bf16 (RNE), relu'd, ranked (ties to the lower index)
+            const uint32_t p01 = relu_bits2(bf16x2_rne(acc[i][j][4 * b], acc[i][j][4 * b + 1]));
+            const uint32_t p23 = relu_bits2(bf16x2_rne(acc[i][j][4 * b + 2], acc[i][j][4 * b + 3]));
+            const Top2 t = top2_keys(p01, p23);
+            codes |= top2_code_of(t) << (8 * b);
+            const float a = __builtin_bit_cast(float, t.first << 16);
+            const float c = __builtin_bit_cast(float, t.second << 16);
+            pair[b] = bf16x2_rne(a * a, c * c);   // s = relu(h)^2 of the kept pair, index order
           }
-          const uint32_t other_codes = __shfl_xor(codes, 32);
+          // metadata byte b = code of group 2b (lane half 0) | code of group
+          // 2b+1 (half 1) << 4; the swap hands half 0 its partner's codes
+          const uint32_t other_codes = __builtin_amdgcn_permlane32_swap(codes, codes, false, false)[1];
           if (ok) {
 #pragma unroll
             for (int b = 0; b < 4; ++b)
               *(uint32_t*)(lv + tl * VP + (fl / 4 + 2 * b + lhalf) * 4) = pair[b];
-            if (lhalf == 0) {
-              uint32_t word = 0;
-#pragma unroll
-              for (int b = 0; b < 4; ++b)
-                word |= (((codes >> (4 * b)) & 0xFu) | (((other_codes >> (4 * b)) & 0xFu) << 4)) << (8 * b);
-              *(uint32_t*)(lm + tl * MP + fl / 8) = word;
-            }
+            if (lhalf == 0) *(uint32_t*)(lm + tl * MP + fl / 8) = codes | (other_codes << 4);
           }
         } else {
           // EPI_DH: scale dS at the kept positions of the stored group by
@@ -747,12 +931,12 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
               for (int q = 0; q < 4; ++q) ds[q] = acc[i][j][4 * b + q];
               const float d0 = i0 == 0u ? ds[0] : i0 == 1u ? ds[1] : ds[2];
               const float d1 = i1 == 1u ? ds[1] : i1 == 2u ? ds[2] : ds[3];
-              const float s0 = bf16_to_f32(sv & 0xFFFFu), s1 = bf16_to_f32(sv >> 16);
-              const float r0 = (float)(__bf16)__builtin_sqrtf(s0);
-              const float r1 = (float)(__bf16)__builtin_sqrtf(s1);
-              const uint32_t o0 = __builtin_bit_cast(uint16_t, (__bf16)(d0 * 2.0f * r0));
-              const uint32_t o1 = __builtin_bit_cast(uint16_t, (__bf16)(d1 * 2.0f * r1));
-              *loc = o0 | (o1 << 16);
+              const float s0 = __builtin_bit_cast(float, sv << 16);
+              const float s1 = __builtin_bit_cast(float, sv & 0xFFFF0000u);
+              const uint32_t rr = bf16x2_rne(sqrt_for_bf16(s0), sqrt_for_bf16(s1));   // relu(h), exact
+              const float r0 = __builtin_bit_cast(float, rr << 16);
+              const float r1 = __builtin_bit_cast(float, rr & 0xFFFF0000u);
+              *loc = bf16x2_rne(d0 * 2.0f * r0, d1 * 2.0f * r1);
             }
           }
         }
