@@ -105,6 +105,19 @@ using CfgSP = GemmCfg<256, 128, 2, 4, OP_SP, OP_K, EPI_BF16, false, 2>;
 template <int AMODE>
 using CfgTT = GemmCfg<256, 256, 4, 2, AMODE, OP_T, EPI_F32, false>;
 
+// Compute units of the current device (cached per device id).
+int device_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
 template <class Cfg>
 hipError_t launch(const char* tag, GemmArgs g, int splits, hipStream_t st) {
   g.tiles_m = (int)cdiv(g.M, Cfg::BM);
@@ -113,7 +126,12 @@ hipError_t launch(const char* tag, GemmArgs g, int splits, hipStream_t st) {
     splits = 1;
     g.k_split = cdiv(g.K, Cfg::BK) * Cfg::BK;
   }
-  const dim3 grid((unsigned)(g.tiles_m * g.tiles_n), (unsigned)splits);
+  // Direct-staged kernels are persistent: one workgroup per CU at most, each
+  // looping over its tiles.
+  const int tiles = g.tiles_m * g.tiles_n;
+  const int cus = device_cus();
+  const int wgs = Cfg::DIRECT && tiles > cus ? cus : tiles;
+  const dim3 grid((unsigned)wgs, (unsigned)splits);
   TimedLaunch tl(tag, st);
   hipLaunchKernelGGL(gemm_kernel<Cfg>, grid, dim3(Cfg::NT), 0, st, g);
   return hipGetLastError();

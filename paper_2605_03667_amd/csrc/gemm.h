@@ -91,14 +91,11 @@ struct GemmArgs {
 };
 
 template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int AMODE_, int BMODE_, int EPI_, bool M_FAST_,
-          int STAGES_ = 2, bool SPREAD_ = false, bool PIPE_ = true>
+          int STAGES_ = 2, bool PIPE_ = true>
 struct GemmCfg {
   // PIPE: double-buffer the MFMA fragments (read sub-step kk+1 during kk's
   // MFMAs); off saves registers.
   static constexpr bool PIPE = PIPE_;
-  // SPREAD: issue the next stage's loads in four parts between the MFMA
-  // sub-steps instead of all at the start of a step.
-  static constexpr bool SPREAD = SPREAD_;
   static constexpr int BM = BM_, BN = BN_, WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
   static constexpr int NW = WAVES_M_ * WAVES_N_, NT = 64 * NW;
   static constexpr int AMODE = AMODE_, BMODE = BMODE_, EPI = EPI_;
@@ -130,7 +127,14 @@ struct GemmCfg {
   static_assert(DIRECT || STAGES_ == 2, "register staging uses two LDS buffers");
   static_assert(!(A_KM || B_KM) || !SPARSE, "2:4 along K with a K-major partner is not used");
   static_assert(STAGES_ == 2 || STAGES_ == 3, "2 or 3 stages");
-  static_assert(STAGES_ * STAGE <= 160 * 1024, "LDS");
+  // The compressed-activation epilogues stage a BN x BM/2 tile of kept values
+  // in one stage buffer and the metadata rows (BM/8 bytes + 4 pad) after the
+  // stages.
+  static constexpr bool STAGED_EPI = EPI_ == EPI_SPARSIFY || EPI_ == EPI_DH;
+  static constexpr int META_PITCH = BM_ / 8 + 4;
+  static constexpr int LDS_BYTES = STAGES_ * STAGE + (STAGED_EPI ? (BN_ * META_PITCH + 15) / 16 * 16 : 0);
+  static_assert(!STAGED_EPI || (BM_ == 256 && BN_ * BM_ <= STAGE && DIRECT), "staged epilogue layout");
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 };
 
 // LDS chunk swizzle.  Fragment reads touch 8 consecutive rows at one chunk;
@@ -419,36 +423,55 @@ __device__ __forceinline__ int xcd_remap(int pid, int total) {
   return (pid % kXcd) * (full / kXcd) + pid / kXcd;
 }
 
+// Persistent schedule of the direct-staged kernels: the grid holds at most
+// one workgroup per CU, and workgroup b runs tiles first, first + stride, ...
+// (< end).  Workgroup ids are dealt to the 8 XCDs round-robin; each XCD gets a
+// contiguous share of the tiles, which its workgroups interleave, so the
+// tiles in flight on one XCD are neighbours sharing operand rows in its L2.
+struct TileRange {
+  int first, stride, end;
+};
+__device__ __forceinline__ TileRange tile_range(int b, int grid, int ntiles) {
+  constexpr int kXcd = 8;
+  if (grid % kXcd != 0) return {b, grid, ntiles};
+  const int x = b % kXcd;
+  const int start = (int)((int64_t)x * ntiles / kXcd), end = (int)((int64_t)(x + 1) * ntiles / kXcd);
+  return {start + b / kXcd, grid / kXcd, end};
+}
+
 template <class Cfg>
 __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
   constexpr int BM = Cfg::BM, BN = Cfg::BN, BK = Cfg::BK, NT = Cfg::NT, NW = Cfg::NW;
   constexpr int FM = Cfg::FM, FN = Cfg::FN, TM = Cfg::TM, TN = Cfg::TN;
   constexpr bool SPARSE = Cfg::SPARSE;
   constexpr int STAGES = Cfg::STAGES;
-  __shared__ __attribute__((aligned(1024))) char smem[STAGES * Cfg::STAGE];
+  __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS_BYTES];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform, so derived LDS bases are scalar
   const int wm = wave / Cfg::WAVES_N, wn = wave % Cfg::WAVES_N;
   const int ntiles = g.tiles_m * g.tiles_n;
-  const int tile = xcd_remap(blockIdx.x, ntiles);
-  const int tm = Cfg::M_FAST ? tile % g.tiles_m : tile / g.tiles_n;
-  const int tn = Cfg::M_FAST ? tile / g.tiles_m : tile % g.tiles_n;
-  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const int64_t kbeg = (int64_t)blockIdx.y * g.k_split;
   const int64_t kend = kbeg + g.k_split < g.K ? kbeg + g.k_split : g.K;
-  const int nsteps = (int)((kend - kbeg + BK - 1) / BK);
+  const int nsteps = kend > kbeg ? (int)((kend - kbeg + BK - 1) / BK) : 0;
+  const int lrow = lane & 31, lhalf = lane >> 5;
+  auto origin = [&](int tile, int64_t& m0, int64_t& n0) __attribute__((always_inline)) {
+    const int tm = Cfg::M_FAST ? tile % g.tiles_m : tile / g.tiles_n;
+    const int tn = Cfg::M_FAST ? tile / g.tiles_m : tile % g.tiles_n;
+    m0 = (int64_t)tm * BM;
+    n0 = (int64_t)tn * BN;
+  };
 
   f32x16 acc[FM][FN];
+  auto zero_acc = [&]() __attribute__((always_inline)) {
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j)
+      for (int j = 0; j < FN; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-
-  const int lrow = lane & 31, lhalf = lane >> 5;
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  };
 
   // MFMAs of one K step on the LDS stage at `base`.  Fragments of sub-step
   // kk+1 are read while sub-step kk's MFMAs run; hook(kk) runs between the
@@ -541,6 +564,279 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     }
   };
 
+  // ---------------------------------------------------------------- epilogues
+  // Writes the tile at (m0, n0); `stage` is an LDS stage buffer that no copy
+  // is filling (the staged epilogues use it).
+  auto epilogue = [&](const int64_t m0, const int64_t n0, char* stage) __attribute__((always_inline)) {
+    if constexpr (Cfg::SWAP) {
+      // Accumulator 4b+q of lane l is C[row l%32][col 8b + 4h + q] of its 32x32
+      // block (h = l / 32).  N is a multiple of 8, so each 8-column (bf16) or
+      // 4-column (fp32) piece is wholly inside or outside the matrix.
+  #pragma unroll
+      for (int i = 0; i < FM; ++i)
+  #pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int64_t row = m0 + wm * TM + i * 32 + lrow;
+          const int64_t colb = n0 + wn * TN + j * 32;
+          if constexpr (Cfg::EPI == EPI_BF16) {
+            // pk[b]: columns 8b+4h .. +3 as two bf16 pairs.  One permlane32 swap
+            // per dword gives lane half 0 columns 0..15 and half 1 columns 16..31.
+            uint32_t pk[4][2];
+  #pragma unroll
+            for (int b = 0; b < 4; ++b)
+  #pragma unroll
+              for (int e = 0; e < 2; ++e)
+                pk[b][e] = bf16x2_rne(acc[i][j][4 * b + 2 * e], acc[i][j][4 * b + 2 * e + 1]);
+            uint32_t out[2][4];
+  #pragma unroll
+            for (int c = 0; c < 2; ++c)
+  #pragma unroll
+              for (int e = 0; e < 2; ++e) {
+                const auto sw = __builtin_amdgcn_permlane32_swap(pk[c][e], pk[c + 2][e], false, false);
+                out[c][e] = sw[0];       // half 0: columns 8c + 2e ..; half 1: 16 + 8c + 2e ..
+                out[c][2 + e] = sw[1];   // half 0: columns 8c + 4 + 2e ..; half 1: 16 + 8c + 4 + 2e ..
+              }
+            const int64_t col = colb + 16 * lhalf;
+            if (row < g.M) {
+              __bf16* dst = (__bf16*)g.C + row * g.ldc + col;
+  #pragma unroll
+              for (int c = 0; c < 2; ++c)
+                if (col + 8 * c < g.N) *(uint4*)(dst + 8 * c) = make_uint4(out[c][0], out[c][1], out[c][2], out[c][3]);
+            }
+          } else {
+            float* part = (float*)g.C + (int64_t)blockIdx.y * g.M * g.N;
+            if (row < g.M) {
+  #pragma unroll
+              for (int b = 0; b < 4; ++b) {
+                const int64_t col = colb + 8 * b + 4 * lhalf;
+                if (col < g.N)
+                  *(float4*)(part + row * g.N + col) =
+                      make_float4(acc[i][j][4 * b], acc[i][j][4 * b + 1], acc[i][j][4 * b + 2], acc[i][j][4 * b + 3]);
+              }
+            }
+          }
+        }
+    } else if constexpr (Cfg::EPI == EPI_BF16) {
+      // 2:4 products (the sparse operand stays the MFMA's first): accumulator
+      // 4b+q of lane l is C[row 8b + 4h + q][col l%32] of its 32x32 block.
+      const bool inside = m0 + BM <= g.M && n0 + BN <= g.N;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int64_t col = n0 + wn * TN + j * 32 + lrow;
+          const int64_t row = m0 + wm * TM + i * 32 + lhalf * 4;
+          __bf16* base = (__bf16*)g.C + row * g.ldc + col;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int dr = (e / 4) * 8 + (e % 4);
+            if (inside || (row + dr < g.M && col < g.N)) base[dr * g.ldc] = (__bf16)acc[i][j][e];
+          }
+        }
+    } else if constexpr (Cfg::EPI == EPI_ACT_DENSE || Cfg::EPI == EPI_DH_DENSE) {
+      // C rows are features f, columns tokens t: accumulators 4b..4b+3 of a
+      // lane are features 8b + 4h + 0..3 of token column l % 32.  Lanes l and
+      // l+32 exchange halves so that each writes 16 contiguous features
+      // (half 0: 0..15, half 1: 16..31 of the 32-row block) of its token row.
+  #pragma unroll
+      for (int i = 0; i < FM; ++i)
+  #pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int64_t t = n0 + wn * TN + j * 32 + lrow;
+          const int64_t f32 = m0 + wm * TM + i * 32;
+          uint2 mine[4];   // block b: features f32 + 8b + 4h .. +3 as 4 bf16
+          if constexpr (Cfg::EPI == EPI_ACT_DENSE) {
+  #pragma unroll
+            for (int b = 0; b < 4; ++b) {
+              uint32_t v[2];
+  #pragma unroll
+              for (int e = 0; e < 2; ++e) {
+                // h rounded to bf16 (RNE), relu'd, squared (act_square) and rounded
+                const uint32_t r = relu_bits2(bf16x2_rne(acc[i][j][4 * b + 2 * e], acc[i][j][4 * b + 2 * e + 1]));
+                if (g.act_square) {
+                  const float lo = __builtin_bit_cast(float, r << 16), hi = __builtin_bit_cast(float, r & 0xFFFF0000u);
+                  v[e] = bf16x2_rne(lo * lo, hi * hi);
+                } else {
+                  v[e] = r;
+                }
+              }
+              mine[b] = make_uint2(v[0], v[1]);
+            }
+          } else {
+  #pragma unroll
+            for (int b = 0; b < 4; ++b) {
+              const int64_t f = f32 + 8 * b + 4 * lhalf;
+              uint2 a = make_uint2(0u, 0u);
+              if (t < g.N && f < g.f_valid) a = *(const uint2*)(g.act + t * g.ld_act + f);
+              uint32_t v[2];
+  #pragma unroll
+              for (int e = 0; e < 2; ++e) {
+                const uint32_t w = e ? a.y : a.x;
+                float x0 = __builtin_bit_cast(float, w << 16), x1 = __builtin_bit_cast(float, w & 0xFFFF0000u);
+                if (g.act_square) {   // r = bf16(sqrt(a)) recovers relu(h) exactly
+                  const uint32_t rr = bf16x2_rne(sqrt_for_bf16(x0), sqrt_for_bf16(x1));
+                  x0 = __builtin_bit_cast(float, rr << 16);
+                  x1 = __builtin_bit_cast(float, rr & 0xFFFF0000u);
+                }
+                v[e] = bf16x2_rne(acc[i][j][4 * b + 2 * e] * 2.0f * x0, acc[i][j][4 * b + 2 * e + 1] * 2.0f * x1);
+              }
+              mine[b] = make_uint2(v[0], v[1]);
+            }
+          }
+          // Half 0 keeps features 0..15 of the block, half 1 features 16..31:
+          // swapping (block 0, block 2) and (block 1, block 3) across the halves
+          // leaves each lane two runs of 8 consecutive features.
+          uint32_t lo[4], hi[4];
+  #pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            const auto s0 = __builtin_amdgcn_permlane32_swap(e ? mine[0].y : mine[0].x, e ? mine[2].y : mine[2].x,
+                                                             false, false);
+            const auto s1 = __builtin_amdgcn_permlane32_swap(e ? mine[1].y : mine[1].x, e ? mine[3].y : mine[3].x,
+                                                             false, false);
+            lo[e] = s0[0];
+            lo[2 + e] = s0[1];
+            hi[e] = s1[0];
+            hi[2 + e] = s1[1];
+          }
+          const int64_t f = f32 + 16 * lhalf;
+          if (t < g.N) {
+            uint16_t* dst = (Cfg::EPI == EPI_ACT_DENSE ? g.act : g.dact) + t * g.ld_act + f;
+            if (f + 8 <= g.f_valid) *(uint4*)dst = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+            if (f + 16 <= g.f_valid) *(uint4*)(dst + 8) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+          }
+        }
+    } else {
+      static_assert(Cfg::STAGED_EPI, "epilogue mode");
+      // C rows are features f, columns tokens t.  Accumulators 4b..4b+3 of a
+      // lane are features 8b + 4h + 0..3 of a 32-row block: one whole group of
+      // 4 (Algorithm 1).  Lanes l and l+32 hold the even and odd groups of the
+      // same 8 features, i.e. the two nibbles of one metadata byte.
+      //
+      // The tile's compressed rows (one per token: BM/2 kept values and BM/8
+      // metadata bytes) are staged in LDS so that global memory sees whole
+      // 16-byte (values) and 8-byte (metadata) pieces of each token row.  The
+      // values go to the stage buffer of the tile's last K step (free once its
+      // MFMAs are done, while the next tile's first loads fill the other one),
+      // with 16-byte chunk c of token row t stored at chunk c ^ (t % 16): the
+      // lanes of a wave, which touch 32 token rows at one column, then spread
+      // over the banks.  Metadata rows (padded by 4 bytes) sit after the stages.
+      constexpr int MP = Cfg::META_PITCH;   // bytes per LDS row of metadata (BM/8 + pad)
+      char* lv = stage;                     // kept values, one BM-byte row per token (chunk-swizzled)
+      char* lm = smem + STAGES * Cfg::STAGE;
+      // byte offset of 4-byte word w of token row t's kept values
+      auto val_word = [](int t, int w) __attribute__((always_inline)) { return t * BM + ((w >> 2) ^ (t & 15)) * 16 + (w & 3) * 4; };
+      const int64_t t_end = g.N - n0;                      // valid tokens in this tile (may exceed BN)
+      const int64_t f_end = g.M - m0;                      // valid features (multiple of 64)
+      __syncthreads();                                     // main-loop LDS reads are finished
+
+      if constexpr (Cfg::EPI == EPI_DH) {
+        // stored S rows of this tile -> LDS
+        constexpr int VCH = BN * (BM / 16);               // 16-byte value chunks
+  #pragma unroll
+        for (int it = 0; it < VCH / NT; ++it) {
+          const int q = it * NT + tid, row = q / (BM / 16), c = q % (BM / 16);
+          if (row < t_end && c * 16 < f_end) {
+            const uint4 v = *(const uint4*)(g.sv + (n0 + row) * g.ldv + m0 / 2 + c * 8);
+            uint32_t* d = (uint32_t*)(lv + row * BM + (c ^ (row & 15)) * 16);
+            d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
+          }
+        }
+        constexpr int MCH = BN * (BM / 64);               // 8-byte metadata chunks
+  #pragma unroll
+        for (int it = 0; it < (MCH + NT - 1) / NT; ++it) {
+          const int q = it * NT + tid, row = q / (BM / 64), c = q % (BM / 64);
+          if (q < MCH && row < t_end && c * 64 < f_end) {
+            const uint2 v = *(const uint2*)(g.sm + (n0 + row) * g.ldm + m0 / 8 + c * 8);
+            uint32_t* d = (uint32_t*)(lm + row * MP + c * 8);
+            d[0] = v.x; d[1] = v.y;
+          }
+        }
+        __syncthreads();
+      }
+
+  #pragma unroll
+      for (int i = 0; i < FM; ++i)
+  #pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int tl = wn * TN + j * 32 + lrow;         // token within the tile
+          const int fl = wm * TM + i * 32;                // first feature of the 32-row block
+          const bool ok = tl < t_end && fl < f_end;
+          uint32_t pair[4], codes = 0;
+          if constexpr (Cfg::EPI == EPI_SPARSIFY) {
+            uint32_t codes = 0;   // code of group b at bits 8b .. 8b+3
+  #pragma unroll
+            for (int b = 0; b < 4; ++b) {
+              // h rounded to bf16 (RNE), relu'd, ranked (ties to the lower index)
+              const uint32_t p01 = relu_bits2(bf16x2_rne(acc[i][j][4 * b], acc[i][j][4 * b + 1]));
+              const uint32_t p23 = relu_bits2(bf16x2_rne(acc[i][j][4 * b + 2], acc[i][j][4 * b + 3]));
+              const Top2 t = top2_keys(p01, p23);
+              codes |= top2_code_of(t) << (8 * b);
+              const float a = __builtin_bit_cast(float, t.first << 16);
+              const float c = __builtin_bit_cast(float, t.second << 16);
+              pair[b] = bf16x2_rne(a * a, c * c);   // s = relu(h)^2 of the kept pair, index order
+            }
+            // metadata byte b = code of group 2b (lane half 0) | code of group
+            // 2b+1 (half 1) << 4; the swap hands half 0 its partner's codes
+            const uint32_t other_codes = __builtin_amdgcn_permlane32_swap(codes, codes, false, false)[1];
+            if (ok) {
+  #pragma unroll
+              for (int b = 0; b < 4; ++b)
+                *(uint32_t*)(lv + val_word(tl, fl / 4 + 2 * b + lhalf)) = pair[b];
+              if (lhalf == 0) *(uint32_t*)(lm + tl * MP + fl / 8) = codes | (other_codes << 4);
+            }
+          } else {
+            // EPI_DH: scale dS at the kept positions of the stored group by
+            // 2 relu(h), relu(h) = bf16(sqrt(s)) exactly; result in place.
+            if (ok) {
+              const uint32_t word = *(const uint32_t*)(lm + tl * MP + fl / 8);
+  #pragma unroll
+              for (int b = 0; b < 4; ++b) {
+                uint32_t* loc = (uint32_t*)(lv + val_word(tl, fl / 4 + 2 * b + lhalf));
+                const uint32_t sv = *loc;
+                const uint32_t code = (word >> (8 * b + 4 * lhalf)) & 0xFu;
+                const uint32_t i0 = code & 3u, i1 = code >> 2;
+                float ds[4];
+  #pragma unroll
+                for (int q = 0; q < 4; ++q) ds[q] = acc[i][j][4 * b + q];
+                const float d0 = i0 == 0u ? ds[0] : i0 == 1u ? ds[1] : ds[2];
+                const float d1 = i1 == 1u ? ds[1] : i1 == 2u ? ds[2] : ds[3];
+                const float s0 = __builtin_bit_cast(float, sv << 16);
+                const float s1 = __builtin_bit_cast(float, sv & 0xFFFF0000u);
+                const uint32_t rr = bf16x2_rne(sqrt_for_bf16(s0), sqrt_for_bf16(s1));   // relu(h), exact
+                const float r0 = __builtin_bit_cast(float, rr << 16);
+                const float r1 = __builtin_bit_cast(float, rr & 0xFFFF0000u);
+                *loc = bf16x2_rne(d0 * 2.0f * r0, d1 * 2.0f * r1);
+              }
+            }
+          }
+        }
+      __syncthreads();
+
+      // LDS -> global: whole 16-byte pieces of each token row
+      uint16_t* dst = Cfg::EPI == EPI_SPARSIFY ? g.sv : g.dv;
+      constexpr int VCH = BN * (BM / 16);
+  #pragma unroll
+      for (int it = 0; it < VCH / NT; ++it) {
+        const int q = it * NT + tid, row = q / (BM / 16), c = q % (BM / 16);
+        if (row < t_end && c * 16 < f_end) {
+          const uint32_t* sp = (const uint32_t*)(lv + row * BM + (c ^ (row & 15)) * 16);
+          *(uint4*)(dst + (n0 + row) * g.ldv + m0 / 2 + c * 8) = make_uint4(sp[0], sp[1], sp[2], sp[3]);
+        }
+      }
+      if constexpr (Cfg::EPI == EPI_SPARSIFY) {
+        constexpr int MCH = BN * (BM / 64);
+  #pragma unroll
+        for (int it = 0; it < (MCH + NT - 1) / NT; ++it) {
+          const int q = it * NT + tid, row = q / (BM / 64), c = q % (BM / 64);
+          if (q < MCH && row < t_end && c * 64 < f_end) {
+            const uint32_t* sp = (const uint32_t*)(lm + row * MP + c * 8);
+            *(uint2*)(g.sm + (n0 + row) * g.ldm + m0 / 8 + c * 8) = make_uint2(sp[0], sp[1]);
+          }
+        }
+      }
+    }
+  };
+
   if constexpr (Cfg::DIRECT) {
     using TA = std::conditional_t<Cfg::A_KM, DmaTileKM<BM, NW>, DmaTile<BM, Cfg::A_ROWB, SPARSE, NW>>;
     using TB = std::conditional_t<Cfg::B_KM, DmaTileKM<BN, NW>, DmaTile<BN, Cfg::B_ROWB, false, NW>>;
@@ -548,8 +844,8 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     constexpr int LA = TA::PER_WAVE, LB = TB::PER_WAVE, LM = SPARSE ? TMeta::PER_WAVE : 0;
     constexpr int LOADS = LA + LB + LM;   // DMA instructions per wave per step
     const uint32_t smem_lds = lds_u32(smem);
-    // Steps of a tile that lies inside both operands take the unchecked path:
-    // per-lane offsets computed once, a scalar base per step.
+    // Per-lane offsets of the unchecked path, relative to a tile's origin:
+    // the same for every tile.
     uint32_t offA[LA], offB[LB], offM[LM > 0 ? LM : 1];
 #pragma unroll
     for (int j = 0; j < LA; ++j) offA[j] = TA::lane_off(j, g.lda, wave, lane);
@@ -561,104 +857,102 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     }
     // Steps [0, steps_in) of a tile inside both operands read no element
     // outside them: their loads skip the bounds checks.
-    int steps_in = 0;
-    if (m0 + BM <= g.m_valid && n0 + BN <= g.N) {
-      const int64_t k_in = (g.ka_valid < g.kb_valid ? g.ka_valid : g.kb_valid) - kbeg;
-      steps_in = k_in <= 0 ? 0 : (int)(k_in / BK < nsteps ? k_in / BK : nsteps);
-    }
-    steps_in = __builtin_amdgcn_readfirstlane(steps_in);
-    // Issue the loads of `step`, part q of 4 (A first half, A second half +
-    // metadata, B first half, B second half), unchecked or checked.
-    auto fast_part = [&](int step, auto q) __attribute__((always_inline)) {
+    auto steps_in_of = [&](int64_t m0, int64_t n0) __attribute__((always_inline)) {
+      int r = 0;
+      if (m0 + BM <= g.m_valid && n0 + BN <= g.N) {
+        const int64_t k_in = (g.ka_valid < g.kb_valid ? g.ka_valid : g.kb_valid) - kbeg;
+        r = k_in <= 0 ? 0 : (int)(k_in / BK < nsteps ? k_in / BK : nsteps);
+      }
+      return __builtin_amdgcn_readfirstlane(r);
+    };
+    // Issue this wave's loads of step `step` of the tile at (m0, n0) into
+    // LDS stage `stage`.
+    auto issue = [&](int64_t m0, int64_t n0, int s_in, int step, int stage) __attribute__((always_inline)) {
       const int64_t k0 = kbeg + (int64_t)step * BK;
-      const uint32_t base = smem_lds + (uint32_t)((step % STAGES) * Cfg::STAGE);
-      constexpr int Q = decltype(q)::value;
-      if constexpr (Q == 0) {
-        TA::template issue_fast<0, LA / 2>(TA::step_base(g.A, g.lda, m0, k0), offA, base, wave);
-      } else if constexpr (Q == 1) {
-        TA::template issue_fast<LA / 2, LA>(TA::step_base(g.A, g.lda, m0, k0), offA, base, wave);
+      const uint32_t base = smem_lds + (uint32_t)(stage * Cfg::STAGE);
+      const uint32_t base_b = base + Cfg::A_BYTES + Cfg::AM_BYTES;
+      if (step < s_in) {
+        TA::template issue_fast<0, LA>(TA::step_base(g.A, g.lda, m0, k0), offA, base, wave);
         if constexpr (SPARSE)
           TMeta::template issue_fast<0, LM>(TMeta::step_base(g.Am, g.ldam, m0, k0), offM, base + Cfg::A_BYTES, wave);
-      } else if constexpr (Q == 2) {
-        TB::template issue_fast<0, LB / 2>(TB::step_base(g.B, g.ldb, n0, k0), offB, base + Cfg::A_BYTES + Cfg::AM_BYTES,
-                                           wave);
+        TB::template issue_fast<0, LB>(TB::step_base(g.B, g.ldb, n0, k0), offB, base_b, wave);
       } else {
-        TB::template issue_fast<LB / 2, LB>(TB::step_base(g.B, g.ldb, n0, k0), offB,
-                                            base + Cfg::A_BYTES + Cfg::AM_BYTES, wave);
-      }
-    };
-    auto slow_part = [&](int step, auto q) __attribute__((always_inline)) {
-      const int64_t k0 = kbeg + (int64_t)step * BK;
-      const uint32_t base = smem_lds + (uint32_t)((step % STAGES) * Cfg::STAGE);
-      constexpr int Q = decltype(q)::value;
-      if constexpr (Q == 0) {
-        TA::template issue<0, LA / 2>(g.A, g.lda, m0, g.m_valid, k0, g.ka_valid, base, wave, lane);
-      } else if constexpr (Q == 1) {
-        TA::template issue<LA / 2, LA>(g.A, g.lda, m0, g.m_valid, k0, g.ka_valid, base, wave, lane);
+        // Checked path (edge tiles, tail steps).  k0 and the lane index pass
+        // through an empty asm so that its addresses are formed afresh here
+        // rather than kept in loop-carried registers across the main loop.
+        int64_t kc = k0;
+        int lc = lane;
+        asm volatile("" : "+s"(kc), "+v"(lc));
+        TA::template issue<0, LA>(g.A, g.lda, m0, g.m_valid, kc, g.ka_valid, base, wave, lc);
         if constexpr (SPARSE)
-          TMeta::template issue<0, LM>(g.Am, g.ldam, m0, g.m_valid, k0, g.ka_valid, base + Cfg::A_BYTES, wave, lane);
-      } else if constexpr (Q == 2) {
-        TB::template issue<0, LB / 2>(g.B, g.ldb, n0, g.N, k0, g.kb_valid, base + Cfg::A_BYTES + Cfg::AM_BYTES,
-                                      wave, lane);
-      } else {
-        TB::template issue<LB / 2, LB>(g.B, g.ldb, n0, g.N, k0, g.kb_valid, base + Cfg::A_BYTES + Cfg::AM_BYTES,
-                                       wave, lane);
+          TMeta::template issue<0, LM>(g.Am, g.ldam, m0, g.m_valid, kc, g.ka_valid, base + Cfg::A_BYTES, wave, lc);
+        TB::template issue<0, LB>(g.B, g.ldb, n0, g.N, kc, g.kb_valid, base_b, wave, lc);
       }
     };
-    auto issue_part = [&](int step, auto q) __attribute__((always_inline)) {
-      if (step < steps_in)
-        fast_part(step, q);
-      else
-        slow_part(step, q);
-    };
-    auto issue_all = [&](int step) __attribute__((always_inline)) {
-      if (step < steps_in) {
-        fast_part(step, std::integral_constant<int, 0>{});
-        fast_part(step, std::integral_constant<int, 1>{});
-        fast_part(step, std::integral_constant<int, 2>{});
-        fast_part(step, std::integral_constant<int, 3>{});
-      } else {
-        slow_part(step, std::integral_constant<int, 0>{});
-        slow_part(step, std::integral_constant<int, 1>{});
-        slow_part(step, std::integral_constant<int, 2>{});
-        slow_part(step, std::integral_constant<int, 3>{});
-      }
-    };
+
+    // Persistent schedule: this workgroup runs tiles first, first + stride,
+    // ... (< end).  Steps are numbered across its tiles (gs = number of the
+    // current tile's step 0) and use stage (gs + s) % STAGES; the loads
+    // STAGES - 1 steps ahead run on into the next tile, so its first loads
+    // are in flight during this tile's last steps and epilogue.
+    const TileRange tr = tile_range(blockIdx.x, gridDim.x, ntiles);
+    if (tr.first >= tr.end) return;
+    int tile = tr.first;
+    int64_t m0, n0;
+    origin(tile, m0, n0);
+    int s_in = steps_in_of(m0, n0);
 #pragma unroll
     for (int p = 0; p < STAGES - 1; ++p)
-      if (p < nsteps) issue_all(p);
-    for (int s = 0; s < nsteps; ++s) {
-      // wait for this wave's loads of step s: the loads of later steps already
-      // issued (at most STAGES - 2 steps) may stay in flight
-      if constexpr (STAGES == 3) {
-        if (s + 1 < nsteps)
-          wait_vmcnt<LOADS>();
-        else
+      if (p < nsteps) issue(m0, n0, s_in, p, p);
+    int gs = 0;
+    for (;;) {
+      const int next = tile + tr.stride;
+      const bool has_next = next < tr.end;
+      int64_t nm0 = 0, nn0 = 0;
+      int ns_in = 0;
+      if (has_next) {
+        origin(next, nm0, nn0);
+        ns_in = steps_in_of(nm0, nn0);
+      }
+      zero_acc();
+      for (int s = 0; s < nsteps; ++s) {
+        // wait for this wave's loads of step s.  At a tile's first step the
+        // previous epilogue's stores are outstanding too: wait for all.  With
+        // three stages the loads of step s + 1 (issued after those of s) may
+        // stay in flight.
+        if constexpr (STAGES == 3) {
+          if (s > 0 && (s + 1 < nsteps || has_next))
+            wait_vmcnt<LOADS>();
+          else
+            wait_vmcnt<0>();
+        } else {
           wait_vmcnt<0>();
-      } else {
-        wait_vmcnt<0>();
-      }
-      lds_barrier();   // every wave's loads of step s landed; step s-1's reads are done
-      const int nxt = s + STAGES - 1;
-      const bool more = nxt < nsteps;
-      if constexpr (!Cfg::SPREAD) {
-        if (more) issue_all(nxt);
-      }
-      compute(smem + (s % STAGES) * Cfg::STAGE, [&](int kk) __attribute__((always_inline)) {
-        if constexpr (Cfg::SPREAD) {
-          if (more) {
-            if (kk == 0) issue_part(nxt, std::integral_constant<int, 0>{});
-            if (kk == 1) issue_part(nxt, std::integral_constant<int, 1>{});
-            if (kk == 2) issue_part(nxt, std::integral_constant<int, 2>{});
-            if (kk == 3) issue_part(nxt, std::integral_constant<int, 3>{});
-          }
         }
-      });
+        lds_barrier();   // every wave's loads of step s landed; step s-1's reads are done
+        // the loads STAGES - 1 steps ahead: of this tile, or of the next one
+        const int la = s + STAGES - 1;
+        const bool here = la < nsteps;
+        if (here || (has_next && la - nsteps < nsteps))
+          issue(here ? m0 : nm0, here ? n0 : nn0, here ? s_in : ns_in, here ? la : la - nsteps, (gs + la) % STAGES);
+        compute(smem + ((gs + s) % STAGES) * Cfg::STAGE, [](int) {});
+      }
+      const int last = nsteps > 0 ? (gs + nsteps - 1) % STAGES : 0;
+      epilogue(m0, n0, smem + last * Cfg::STAGE);
+      if (!has_next) break;
+      gs += nsteps;
+      tile = next;
+      m0 = nm0;
+      n0 = nn0;
+      s_in = ns_in;
     }
   } else {
-    // A: the 2:4 K-major operand, expanded in registers; B: DMA.  The next
-    // step's A loads and B DMA are issued before the current step's MFMAs; A
-    // is written to LDS after them; one barrier per step.
+    // A: the 2:4 K-major operand, expanded in registers; B: DMA.  One tile
+    // per workgroup.  The next step's A loads and B DMA are issued before the
+    // current step's MFMAs; A is written to LDS after them; one barrier per
+    // step.
+    int64_t m0, n0;
+    origin(xcd_remap(blockIdx.x, ntiles), m0, n0);
+    zero_acc();
     StagerKMSP<BM, NT> sa;
     using TB = std::conditional_t<Cfg::B_KM, DmaTileKM<BN, NW>, DmaTile<BN, Cfg::B_ROWB, false, NW>>;
     const uint32_t smem_lds = lds_u32(smem);
@@ -696,275 +990,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       if (more) sa.store(smem + (buf ^ 1) * Cfg::STAGE, tid);
       __syncthreads();   // A's LDS writes and B's DMA of step s+1 are complete
     }
-  }
-
-  // ---------------------------------------------------------------- epilogues
-  if constexpr (Cfg::SWAP) {
-    // Accumulator 4b+q of lane l is C[row l%32][col 8b + 4h + q] of its 32x32
-    // block (h = l / 32).  N is a multiple of 8, so each 8-column (bf16) or
-    // 4-column (fp32) piece is wholly inside or outside the matrix.
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int64_t row = m0 + wm * TM + i * 32 + lrow;
-        const int64_t colb = n0 + wn * TN + j * 32;
-        if constexpr (Cfg::EPI == EPI_BF16) {
-          // pk[b]: columns 8b+4h .. +3 as two bf16 pairs.  One permlane32 swap
-          // per dword gives lane half 0 columns 0..15 and half 1 columns 16..31.
-          uint32_t pk[4][2];
-#pragma unroll
-          for (int b = 0; b < 4; ++b)
-#pragma unroll
-            for (int e = 0; e < 2; ++e)
-              pk[b][e] = bf16x2_rne(acc[i][j][4 * b + 2 * e], acc[i][j][4 * b + 2 * e + 1]);
-          uint32_t out[2][4];
-#pragma unroll
-          for (int c = 0; c < 2; ++c)
-#pragma unroll
-            for (int e = 0; e < 2; ++e) {
-              const auto sw = __builtin_amdgcn_permlane32_swap(pk[c][e], pk[c + 2][e], false, false);
-              out[c][e] = sw[0];       // half 0: columns 8c + 2e ..; half 1: 16 + 8c + 2e ..
-              out[c][2 + e] = sw[1];   // half 0: columns 8c + 4 + 2e ..; half 1: 16 + 8c + 4 + 2e ..
-            }
-          const int64_t col = colb + 16 * lhalf;
-          if (row < g.M) {
-            __bf16* dst = (__bf16*)g.C + row * g.ldc + col;
-#pragma unroll
-            for (int c = 0; c < 2; ++c)
-              if (col + 8 * c < g.N) *(uint4*)(dst + 8 * c) = make_uint4(out[c][0], out[c][1], out[c][2], out[c][3]);
-          }
-        } else {
-          float* part = (float*)g.C + (int64_t)blockIdx.y * g.M * g.N;
-          if (row < g.M) {
-#pragma unroll
-            for (int b = 0; b < 4; ++b) {
-              const int64_t col = colb + 8 * b + 4 * lhalf;
-              if (col < g.N)
-                *(float4*)(part + row * g.N + col) =
-                    make_float4(acc[i][j][4 * b], acc[i][j][4 * b + 1], acc[i][j][4 * b + 2], acc[i][j][4 * b + 3]);
-            }
-          }
-        }
-      }
-  } else if constexpr (Cfg::EPI == EPI_BF16 || Cfg::EPI == EPI_F32) {
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int64_t col = n0 + wn * TN + j * 32 + lrow;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int64_t row = m0 + wm * TM + i * 32 + (e / 4) * 8 + lhalf * 4 + (e % 4);
-          if (row < g.M && col < g.N) {
-            if constexpr (Cfg::EPI == EPI_BF16) {
-              const __bf16 v = (__bf16)acc[i][j][e];
-              ((__bf16*)g.C)[row * g.ldc + col] = v;
-            } else {
-              float* part = (float*)g.C + (int64_t)blockIdx.y * g.M * g.N;
-              part[row * g.N + col] = acc[i][j][e];
-            }
-          }
-        }
-      }
-  } else if constexpr (Cfg::EPI == EPI_ACT_DENSE || Cfg::EPI == EPI_DH_DENSE) {
-    // C rows are features f, columns tokens t: accumulators 4b..4b+3 of a
-    // lane are features 8b + 4h + 0..3 of token column l % 32.  Lanes l and
-    // l+32 exchange halves so that each writes 16 contiguous features
-    // (half 0: 0..15, half 1: 16..31 of the 32-row block) of its token row.
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int64_t t = n0 + wn * TN + j * 32 + lrow;
-        const int64_t f32 = m0 + wm * TM + i * 32;
-        uint2 mine[4];   // block b: features f32 + 8b + 4h .. +3 as 4 bf16
-        if constexpr (Cfg::EPI == EPI_ACT_DENSE) {
-#pragma unroll
-          for (int b = 0; b < 4; ++b) {
-            uint32_t v[2];
-#pragma unroll
-            for (int e = 0; e < 2; ++e) {
-              // h rounded to bf16 (RNE), relu'd, squared (act_square) and rounded
-              const uint32_t r = relu_bits2(bf16x2_rne(acc[i][j][4 * b + 2 * e], acc[i][j][4 * b + 2 * e + 1]));
-              if (g.act_square) {
-                const float lo = __builtin_bit_cast(float, r << 16), hi = __builtin_bit_cast(float, r & 0xFFFF0000u);
-                v[e] = bf16x2_rne(lo * lo, hi * hi);
-              } else {
-                v[e] = r;
-              }
-            }
-            mine[b] = make_uint2(v[0], v[1]);
-          }
-        } else {
-#pragma unroll
-          for (int b = 0; b < 4; ++b) {
-            const int64_t f = f32 + 8 * b + 4 * lhalf;
-            uint2 a = make_uint2(0u, 0u);
-            if (t < g.N && f < g.f_valid) a = *(const uint2*)(g.act + t * g.ld_act + f);
-            uint32_t v[2];
-#pragma unroll
-            for (int e = 0; e < 2; ++e) {
-              const uint32_t w = e ? a.y : a.x;
-              float x0 = __builtin_bit_cast(float, w << 16), x1 = __builtin_bit_cast(float, w & 0xFFFF0000u);
-              if (g.act_square) {   // r = bf16(sqrt(a)) recovers relu(h) exactly
-                const uint32_t rr = bf16x2_rne(sqrt_for_bf16(x0), sqrt_for_bf16(x1));
-                x0 = __builtin_bit_cast(float, rr << 16);
-                x1 = __builtin_bit_cast(float, rr & 0xFFFF0000u);
-              }
-              v[e] = bf16x2_rne(acc[i][j][4 * b + 2 * e] * 2.0f * x0, acc[i][j][4 * b + 2 * e + 1] * 2.0f * x1);
-            }
-            mine[b] = make_uint2(v[0], v[1]);
-          }
-        }
-        // Half 0 keeps features 0..15 of the block, half 1 features 16..31:
-        // swapping (block 0, block 2) and (block 1, block 3) across the halves
-        // leaves each lane two runs of 8 consecutive features.
-        uint32_t lo[4], hi[4];
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          const auto s0 = __builtin_amdgcn_permlane32_swap(e ? mine[0].y : mine[0].x, e ? mine[2].y : mine[2].x,
-                                                           false, false);
-          const auto s1 = __builtin_amdgcn_permlane32_swap(e ? mine[1].y : mine[1].x, e ? mine[3].y : mine[3].x,
-                                                           false, false);
-          lo[e] = s0[0];
-          lo[2 + e] = s0[1];
-          hi[e] = s1[0];
-          hi[2 + e] = s1[1];
-        }
-        const int64_t f = f32 + 16 * lhalf;
-        if (t < g.N) {
-          uint16_t* dst = (Cfg::EPI == EPI_ACT_DENSE ? g.act : g.dact) + t * g.ld_act + f;
-          if (f + 8 <= g.f_valid) *(uint4*)dst = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-          if (f + 16 <= g.f_valid) *(uint4*)(dst + 8) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-        }
-      }
-  } else {
-    // C rows are features f, columns tokens t.  Accumulators 4b..4b+3 of a
-    // lane are features 8b + 4h + 0..3 of a 32-row block: one whole group of
-    // 4 (Algorithm 1).  Lanes l and l+32 hold the even and odd groups of the
-    // same 8 features, i.e. the two nibbles of one metadata byte.
-    //
-    // The tile's compressed rows (one per token: BM/2 kept values and BM/8
-    // metadata bytes) are staged in LDS so that global memory sees whole
-    // 16-byte (values) and 8-byte (metadata) pieces of each token row.  LDS
-    // rows are padded by 4 bytes so that the 32 lanes of a wave, which touch
-    // 32 different token rows at one column, hit 32 different banks.
-    constexpr int VP = BM + 4;            // bytes per LDS row of kept values (BM/2 bf16 + pad)
-    constexpr int MP = BM / 8 + 4;        // bytes per LDS row of metadata
-    constexpr int META_OFF = (BN * VP + 15) / 16 * 16;
-    static_assert(META_OFF + BN * MP <= STAGES * Cfg::STAGE, "epilogue staging fits in LDS");
-    char* lv = smem;
-    char* lm = smem + META_OFF;
-    const int64_t t_end = g.N - n0;                      // valid tokens in this tile (may exceed BN)
-    const int64_t f_end = g.M - m0;                      // valid features (multiple of 64)
-    __syncthreads();                                     // main-loop LDS reads are finished
-
-    if constexpr (Cfg::EPI == EPI_DH) {
-      // stored S rows of this tile -> LDS
-      constexpr int VCH = BN * (BM / 16);               // 16-byte value chunks
-#pragma unroll
-      for (int it = 0; it < VCH / NT; ++it) {
-        const int q = it * NT + tid, row = q / (BM / 16), c = q % (BM / 16);
-        if (row < t_end && c * 16 < f_end) {
-          const uint4 v = *(const uint4*)(g.sv + (n0 + row) * g.ldv + m0 / 2 + c * 8);
-          uint32_t* d = (uint32_t*)(lv + row * VP + c * 16);
-          d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
-        }
-      }
-      constexpr int MCH = BN * (BM / 64);               // 8-byte metadata chunks
-#pragma unroll
-      for (int it = 0; it < (MCH + NT - 1) / NT; ++it) {
-        const int q = it * NT + tid, row = q / (BM / 64), c = q % (BM / 64);
-        if (q < MCH && row < t_end && c * 64 < f_end) {
-          const uint2 v = *(const uint2*)(g.sm + (n0 + row) * g.ldm + m0 / 8 + c * 8);
-          uint32_t* d = (uint32_t*)(lm + row * MP + c * 8);
-          d[0] = v.x; d[1] = v.y;
-        }
-      }
-      __syncthreads();
-    }
-
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int tl = wn * TN + j * 32 + lrow;         // token within the tile
-        const int fl = wm * TM + i * 32;                // first feature of the 32-row block
-        const bool ok = tl < t_end && fl < f_end;
-        uint32_t pair[4], codes = 0;
-        if constexpr (Cfg::EPI == EPI_SPARSIFY) {
-          uint32_t codes = 0;   // code of group b at bits 8b .. 8b+3
-#pragma unroll
-          for (int b = 0; b < 4; ++b) {
-            // h rounded to bf16 (RNE), relu'd, ranked (ties to the lower index)
-            const uint32_t p01 = relu_bits2(bf16x2_rne(acc[i][j][4 * b], acc[i][j][4 * b + 1]));
-            const uint32_t p23 = relu_bits2(bf16x2_rne(acc[i][j][4 * b + 2], acc[i][j][4 * b + 3]));
-            const Top2 t = top2_keys(p01, p23);
-            codes |= top2_code_of(t) << (8 * b);
-            const float a = __builtin_bit_cast(float, t.first << 16);
-            const float c = __builtin_bit_cast(float, t.second << 16);
-            pair[b] = bf16x2_rne(a * a, c * c);   // s = relu(h)^2 of the kept pair, index order
-          }
-          // metadata byte b = code of group 2b (lane half 0) | code of group
-          // 2b+1 (half 1) << 4; the swap hands half 0 its partner's codes
-          const uint32_t other_codes = __builtin_amdgcn_permlane32_swap(codes, codes, false, false)[1];
-          if (ok) {
-#pragma unroll
-            for (int b = 0; b < 4; ++b)
-              *(uint32_t*)(lv + tl * VP + (fl / 4 + 2 * b + lhalf) * 4) = pair[b];
-            if (lhalf == 0) *(uint32_t*)(lm + tl * MP + fl / 8) = codes | (other_codes << 4);
-          }
-        } else {
-          // EPI_DH: scale dS at the kept positions of the stored group by
-          // 2 relu(h), relu(h) = bf16(sqrt(s)) exactly; result in place.
-          if (ok) {
-            const uint32_t word = *(const uint32_t*)(lm + tl * MP + fl / 8);
-#pragma unroll
-            for (int b = 0; b < 4; ++b) {
-              uint32_t* loc = (uint32_t*)(lv + tl * VP + (fl / 4 + 2 * b + lhalf) * 4);
-              const uint32_t sv = *loc;
-              const uint32_t code = (word >> (8 * b + 4 * lhalf)) & 0xFu;
-              const uint32_t i0 = code & 3u, i1 = code >> 2;
-              float ds[4];
-#pragma unroll
-              for (int q = 0; q < 4; ++q) ds[q] = acc[i][j][4 * b + q];
-              const float d0 = i0 == 0u ? ds[0] : i0 == 1u ? ds[1] : ds[2];
-              const float d1 = i1 == 1u ? ds[1] : i1 == 2u ? ds[2] : ds[3];
-              const float s0 = __builtin_bit_cast(float, sv << 16);
-              const float s1 = __builtin_bit_cast(float, sv & 0xFFFF0000u);
-              const uint32_t rr = bf16x2_rne(sqrt_for_bf16(s0), sqrt_for_bf16(s1));   // relu(h), exact
-              const float r0 = __builtin_bit_cast(float, rr << 16);
-              const float r1 = __builtin_bit_cast(float, rr & 0xFFFF0000u);
-              *loc = bf16x2_rne(d0 * 2.0f * r0, d1 * 2.0f * r1);
-            }
-          }
-        }
-      }
-    __syncthreads();
-
-    // LDS -> global: whole 16-byte pieces of each token row
-    uint16_t* dst = Cfg::EPI == EPI_SPARSIFY ? g.sv : g.dv;
-    constexpr int VCH = BN * (BM / 16);
-#pragma unroll
-    for (int it = 0; it < VCH / NT; ++it) {
-      const int q = it * NT + tid, row = q / (BM / 16), c = q % (BM / 16);
-      if (row < t_end && c * 16 < f_end) {
-        const uint32_t* sp = (const uint32_t*)(lv + row * VP + c * 16);
-        *(uint4*)(dst + (n0 + row) * g.ldv + m0 / 2 + c * 8) = make_uint4(sp[0], sp[1], sp[2], sp[3]);
-      }
-    }
-    if constexpr (Cfg::EPI == EPI_SPARSIFY) {
-      constexpr int MCH = BN * (BM / 64);
-#pragma unroll
-      for (int it = 0; it < (MCH + NT - 1) / NT; ++it) {
-        const int q = it * NT + tid, row = q / (BM / 64), c = q % (BM / 64);
-        if (q < MCH && row < t_end && c * 64 < f_end) {
-          const uint32_t* sp = (const uint32_t*)(lm + row * MP + c * 8);
-          *(uint2*)(g.sm + (n0 + row) * g.ldm + m0 / 8 + c * 8) = make_uint2(sp[0], sp[1]);
-        }
-      }
-    }
+    epilogue(m0, n0, smem);
   }
 }
 
