@@ -55,27 +55,54 @@ hipError_t transpose_pad(const uint16_t* in, int64_t rows, int64_t cols, int64_t
   return hipGetLastError();
 }
 
-// out = sum over splits of part[s] (fixed order, so the result is
-// deterministic); rows m < rows_out only; optionally transposed.
+// out[m][n] (or out[n][m] when transposing) = sum over the splits k, in order
+// (so the result is deterministic), of part[k][m][n], for rows m < rows_out.  One 64 x 64 (m, n) tile per block:
+// thread (ty, tx) sums float4 columns n0 + 4 tx of rows m0 + ty + 16 i.  N and
+// a non-transposed ldo are multiples of 4 (the model dimensions are multiples
+// of 8); the transposed tile goes through LDS so that its stores run along m.
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int splits, int64_t M,
-                                                            int64_t N, int64_t rows_out, int transpose,
-                                                            float* __restrict__ out, int64_t ldo) {
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e >= rows_out * N) return;
-  int64_t m, n;
-  if (transpose) {   // consecutive threads walk m so the transposed writes are contiguous
-    n = e / rows_out;
-    m = e - n * rows_out;
-  } else {
-    m = e / N;
-    n = e - m * N;
+                                                           int64_t N, int64_t rows_out, int transpose,
+                                                           float* __restrict__ out, int64_t ldo) {
+  __shared__ float tile[64][65];
+  const int64_t m0 = (int64_t)blockIdx.y * 64, n0 = (int64_t)blockIdx.x * 64;
+  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+  const int64_t n = n0 + 4 * tx;
+  float4 acc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int k = 0; k < splits; ++k) {
+    const float* pk = part + (int64_t)k * M * N;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t m = m0 + ty + 16 * i;
+      if (m < rows_out && n < N) {
+        const float4 v = *(const float4*)(pk + m * N + n);
+        acc[i].x += v.x; acc[i].y += v.y; acc[i].z += v.z; acc[i].w += v.w;
+      }
+    }
   }
-  float s = 0.f;
-  for (int k = 0; k < splits; ++k) s += part[(int64_t)k * M * N + m * N + n];
-  if (transpose)
-    out[n * ldo + m] = s;
-  else
-    out[m * ldo + n] = s;
+  if (!transpose) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t m = m0 + ty + 16 * i;
+      if (m < rows_out && n < N) *(float4*)(out + m * ldo + n) = acc[i];
+    }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    tile[4 * tx + 0][ty + 16 * i] = acc[i].x;
+    tile[4 * tx + 1][ty + 16 * i] = acc[i].y;
+    tile[4 * tx + 2][ty + 16 * i] = acc[i].z;
+    tile[4 * tx + 3][ty + 16 * i] = acc[i].w;
+  }
+  __syncthreads();
+  // out row n0 + r, columns m0 + c: consecutive threads take consecutive m
+  for (int q = threadIdx.x; q < 64 * 64; q += 256) {
+    const int r = q / 64, c = q % 64;
+    const int64_t on = n0 + r, om = m0 + c;
+    if (on < N && om < rows_out) out[on * ldo + om] = tile[r][c];
+  }
 }
 
 __global__ __launch_bounds__(256) void fill_zero_kernel(float* __restrict__ p, int64_t n) {
@@ -184,10 +211,9 @@ hipError_t gemm_tt_f32(const char* tag, const uint16_t* A, int64_t lda, const ui
   g.k_split = p.k_split; g.C = part; g.ldc = N;
   hipError_t e = launch<CfgTT<AMODE>>(tag, g, p.splits, st);
   if (e != hipSuccess) return e;
-  const int64_t n_out = rows_out * N;
   TimedLaunch tl("splitk_reduce", st);
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)cdiv(n_out, 256)), dim3(256), 0, st, part, p.splits,
-                     M, N, rows_out, transpose ? 1 : 0, out, ldo);
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)cdiv(N, 64), (unsigned)cdiv(rows_out, 64)), dim3(256), 0, st,
+                     part, p.splits, M, N, rows_out, transpose ? 1 : 0, out, ldo);
   return hipGetLastError();
 }
 

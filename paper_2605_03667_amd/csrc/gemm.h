@@ -977,6 +977,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, kbeg, g.ka_valid, tid);
       issue_b(0);
       sa.store(smem, tid);
+      wait_vmcnt<0>();
       __syncthreads();
     }
     for (int s = 0; s < nsteps; ++s) {
@@ -988,6 +989,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       }
       compute(smem + buf * Cfg::STAGE, [](int) {});
       if (more) sa.store(smem + (buf ^ 1) * Cfg::STAGE, tid);
+      wait_vmcnt<0>();   // B's DMA of step s+1 has landed
       __syncthreads();   // A's LDS writes and B's DMA of step s+1 are complete
     }
     epilogue(m0, n0, smem);
