@@ -55,11 +55,41 @@ hipError_t transpose_pad(const uint16_t* in, int64_t rows, int64_t cols, int64_t
   return hipGetLastError();
 }
 
-// out[m][n] (or out[n][m] when transposing) = sum over the splits k, in order
-// (so the result is deterministic), of part[k][m][n], for rows m < rows_out.  One 64 x 64 (m, n) tile per block:
-// thread (ty, tx) sums float4 columns n0 + 4 tx of rows m0 + ty + 16 i.  N and
-// a non-transposed ldo are multiples of 4 (the model dimensions are multiples
-// of 8); the transposed tile goes through LDS so that its stores run along m.
+// Writes a 64 x 64 (m, n) tile of sums held as acc[i] = row m0 + ty + 16 i,
+// float4 columns n0 + 4 tx: to out[m][n], or to out[n][m] when transposing
+// (through LDS, so that consecutive threads store consecutive m).  N and a
+// non-transposed ldo are multiples of 4 (the model dimensions are multiples
+// of 8).
+__device__ __forceinline__ void reduce_store(const float4 (&acc)[4], int64_t m0, int64_t n0, int tx, int ty,
+                                             int64_t N, int64_t rows_out, int transpose, float* __restrict__ out,
+                                             int64_t ldo, float (*tile)[65]) {
+  const int64_t n = n0 + 4 * tx;
+  if (!transpose) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t m = m0 + ty + 16 * i;
+      if (m < rows_out && n < N) *(float4*)(out + m * ldo + n) = acc[i];
+    }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    tile[4 * tx + 0][ty + 16 * i] = acc[i].x;
+    tile[4 * tx + 1][ty + 16 * i] = acc[i].y;
+    tile[4 * tx + 2][ty + 16 * i] = acc[i].z;
+    tile[4 * tx + 3][ty + 16 * i] = acc[i].w;
+  }
+  __syncthreads();
+  for (int q = threadIdx.x; q < 64 * 64; q += 256) {
+    const int r = q / 64, c = q % 64;
+    const int64_t on = n0 + r, om = m0 + c;
+    if (on < N && om < rows_out) out[on * ldo + om] = tile[r][c];
+  }
+}
+
+// out[m][n] (or out[n][m]) = sum over the splits k, in order (so the result
+// is deterministic), of part[k][m][n], for rows m < rows_out; one 64 x 64
+// (m, n) tile per block.
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int splits, int64_t M,
                                                            int64_t N, int64_t rows_out, int transpose,
                                                            float* __restrict__ out, int64_t ldo) {
@@ -81,28 +111,43 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
       }
     }
   }
-  if (!transpose) {
+  reduce_store(acc, m0, n0, tx, ty, N, rows_out, transpose, out, ldo, tile);
+}
+
+// The stream-K counterpart: workgroup w of `wgs` owns iterations
+// [w I / wgs, (w+1) I / wgs) of the I = ntiles x S (tile, K step) space and
+// wrote the partial of the j-th tile it touched to part + (w segs + j) 256^2
+// (256 x 256 row-major).  The sums run over the workgroups in order, i.e. in
+// K order, so the result is deterministic.
+__global__ __launch_bounds__(256) void streamk_reduce_kernel(const float* __restrict__ part, int wgs, int segs,
+                                                            int64_t S, int tiles_n, int64_t ntiles, int64_t N,
+                                                            int64_t rows_out, int transpose, float* __restrict__ out,
+                                                            int64_t ldo) {
+  __shared__ float tile[64][65];
+  const int64_t m0 = (int64_t)blockIdx.y * 64, n0 = (int64_t)blockIdx.x * 64;
+  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+  const int64_t t = (m0 / 256) * tiles_n + n0 / 256;
+  const int lm = (int)(m0 % 256), ln = (int)(n0 % 256) + 4 * tx;
+  const int64_t I = ntiles * S, tb = t * S, te = tb + S;
+  auto beg_of = [&](int64_t w) { return w * I / wgs; };
+  int64_t w = tb * wgs / I;   // the workgroup whose range holds iteration tb
+  while (w > 0 && beg_of(w) > tb) --w;
+  while (beg_of(w + 1) <= tb) ++w;
+  float4 acc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (; w < wgs; ++w) {
+    const int64_t b = beg_of(w), e = beg_of(w + 1);
+    if (b >= te) break;
+    if (e <= b) continue;
+    const float* slot = part + ((int64_t)w * segs + (t - b / S)) * 65536;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int64_t m = m0 + ty + 16 * i;
-      if (m < rows_out && n < N) *(float4*)(out + m * ldo + n) = acc[i];
+      const float4 v = *(const float4*)(slot + (int64_t)(lm + ty + 16 * i) * 256 + ln);
+      acc[i].x += v.x; acc[i].y += v.y; acc[i].z += v.z; acc[i].w += v.w;
     }
-    return;
   }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    tile[4 * tx + 0][ty + 16 * i] = acc[i].x;
-    tile[4 * tx + 1][ty + 16 * i] = acc[i].y;
-    tile[4 * tx + 2][ty + 16 * i] = acc[i].z;
-    tile[4 * tx + 3][ty + 16 * i] = acc[i].w;
-  }
-  __syncthreads();
-  // out row n0 + r, columns m0 + c: consecutive threads take consecutive m
-  for (int q = threadIdx.x; q < 64 * 64; q += 256) {
-    const int r = q / 64, c = q % 64;
-    const int64_t on = n0 + r, om = m0 + c;
-    if (on < N && om < rows_out) out[on * ldo + om] = tile[r][c];
-  }
+  reduce_store(acc, m0, n0, tx, ty, N, rows_out, transpose, out, ldo, tile);
 }
 
 __global__ __launch_bounds__(256) void fill_zero_kernel(float* __restrict__ p, int64_t n) {
@@ -174,25 +219,37 @@ hipError_t gemm_nt_bf16(const char* tag, const uint16_t* A, int64_t lda, const u
   return launch<CfgNT<256, EPI_BF16, false>>(tag, g, 1, st);
 }
 
-// Split plan of a K = T product: enough workgroups to cover the 256 CUs once,
-// each split at least 8 K steps long.  (More splits fill the CUs more evenly
-// but cost more partial-sum traffic than they save at the 1B shapes.)
+// Work split of a K = T product.  Split-K: enough workgroups to cover the 256
+// CUs once, each split at least 8 K steps long (more splits fill the CUs more
+// evenly but cost more partial-sum traffic than they save at the 1B shapes).
+// When that leaves more than a tenth of the CUs idle, the register-staged
+// (2:4) products use stream-K instead: 256 workgroups with equal shares of
+// the tiles x K steps, each at least 8 steps.
+constexpr int kStreamWgs = 256;
 struct SplitPlan {
   int splits;
   int64_t k_split;
+  int64_t stream_steps;   // > 0: stream-K with this many K steps per tile
+  int segs;               // stream-K partial tiles per workgroup
 };
-SplitPlan plan_splits(int64_t M, int64_t N, int64_t K) {
-  if (K <= 0) return {0, 0};
+SplitPlan plan_splits(int64_t M, int64_t N, int64_t K, bool allow_stream) {
+  if (K <= 0) return {0, 0, 0, 0};
   const int64_t tiles = cdiv(M, 256) * cdiv(N, 256);
   const int64_t steps = cdiv(K, 64);
   int64_t s = 256 / tiles;
   if (s < 1) s = 1;
   if (s > steps / 8) s = steps / 8 > 0 ? steps / 8 : 1;
   const int64_t k_split = cdiv(cdiv(K, s), 64) * 64;
-  return {(int)cdiv(K, k_split), k_split};
+  const int splits = (int)cdiv(K, k_split);
+  if (allow_stream && tiles * splits * 10 < 9LL * kStreamWgs && tiles * steps >= 8LL * kStreamWgs) {
+    const int64_t longest = cdiv(tiles * steps, kStreamWgs);
+    return {1, K, steps, (int)((longest - 1) / steps + 2)};
+  }
+  return {splits, k_split, 0, 0};
 }
-size_t partial_bytes(int64_t M, int64_t N, int64_t K) {
-  const SplitPlan p = plan_splits(M, N, K);
+size_t partial_bytes(int64_t M, int64_t N, int64_t K, bool allow_stream) {
+  const SplitPlan p = plan_splits(M, N, K, allow_stream);
+  if (p.stream_steps > 0) return (size_t)kStreamWgs * p.segs * 256 * 256 * sizeof(float);
   return (size_t)p.splits * M * N * sizeof(float);
 }
 
@@ -204,16 +261,35 @@ hipError_t gemm_tt_f32(const char* tag, const uint16_t* A, int64_t lda, const ui
                        int64_t ldb, int64_t M, int64_t N, int64_t K, float* part, float* out, int64_t rows_out,
                        bool transpose, int64_t ldo, hipStream_t st) {
   if (K == 0) return hipSuccess;
-  const SplitPlan p = plan_splits(M, N, K);
+  using Cfg = CfgTT<AMODE>;
+  const SplitPlan p = plan_splits(M, N, K, AMODE == OP_TSP);
   GemmArgs g{};
   g.A = A; g.lda = lda; g.Am = Am; g.ldam = ldam; g.B = B; g.ldb = ldb;
   g.M = M; g.N = N; g.K = K; g.m_valid = M; g.ka_valid = K; g.kb_valid = K;
   g.k_split = p.k_split; g.C = part; g.ldc = N;
-  hipError_t e = launch<CfgTT<AMODE>>(tag, g, p.splits, st);
+  const dim3 rgrid((unsigned)cdiv(N, 64), (unsigned)cdiv(rows_out, 64));
+  if (p.stream_steps > 0) {
+    static_assert(Cfg::BM == 256 && Cfg::BN == 256, "stream-K partial tiles are 256 x 256");
+    g.stream_steps = p.stream_steps;
+    g.stream_segs = p.segs;
+    g.tiles_m = (int)cdiv(M, Cfg::BM);
+    g.tiles_n = (int)cdiv(N, Cfg::BN);
+    {
+      TimedLaunch tl(tag, st);
+      hipLaunchKernelGGL(gemm_kernel<Cfg>, dim3(kStreamWgs), dim3(Cfg::NT), 0, st, g);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    TimedLaunch tl("splitk_reduce", st);
+    hipLaunchKernelGGL(streamk_reduce_kernel, rgrid, dim3(256), 0, st, part, kStreamWgs, p.segs, p.stream_steps,
+                       g.tiles_n, (int64_t)g.tiles_m * g.tiles_n, N, rows_out, transpose ? 1 : 0, out, ldo);
+    return hipGetLastError();
+  }
+  hipError_t e = launch<Cfg>(tag, g, p.splits, st);
   if (e != hipSuccess) return e;
   TimedLaunch tl("splitk_reduce", st);
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)cdiv(N, 64), (unsigned)cdiv(rows_out, 64)), dim3(256), 0, st,
-                     part, p.splits, M, N, rows_out, transpose ? 1 : 0, out, ldo);
+  hipLaunchKernelGGL(splitk_reduce_kernel, rgrid, dim3(256), 0, st, part, p.splits, M, N, rows_out,
+                     transpose ? 1 : 0, out, ldo);
   return hipGetLastError();
 }
 
@@ -254,8 +330,8 @@ BwdWs bwd_ws(char* p, int64_t T, int64_t d, int64_t F, int64_t r, bool dense, bo
   }
   // split-K partials of the products over tokens (d_ff-wide ones have Fp rows
   // when read compressed, F rows when dense)
-  size_t pb = partial_bytes(r, d, T);
-  const size_t p2 = partial_bytes(Fp, r, T), p3 = partial_bytes(d, r, T), p4 = partial_bytes(F, r, T);
+  size_t pb = partial_bytes(r, d, T, false);
+  const size_t p2 = partial_bytes(Fp, r, T, true), p3 = partial_bytes(d, r, T, false), p4 = partial_bytes(F, r, T, false);
   if (p2 > pb) pb = p2;
   if (p3 > pb) pb = p3;
   if (p4 > pb) pb = p4;

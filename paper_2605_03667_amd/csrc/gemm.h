@@ -88,6 +88,12 @@ struct GemmArgs {
   int64_t f_valid;
   int act_square;
   int tiles_m, tiles_n;
+  // Stream-K (register-staged path, EPI_F32): when stream_steps > 0, the
+  // gridDim.x workgroups split the tiles x stream_steps K steps into equal
+  // contiguous ranges; workgroup w writes the partial tile of the j-th tile
+  // its range touches to C + (w * stream_segs + j) * BM * BN (row-major).
+  int64_t stream_steps;
+  int stream_segs;
 };
 
 template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int AMODE_, int BMODE_, int EPI_, bool M_FAST_,
@@ -566,15 +572,17 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
 
   // ---------------------------------------------------------------- epilogues
   // Writes the tile at (m0, n0); `stage` is an LDS stage buffer that no copy
-  // is filling (the staged epilogues use it).
+  // is filling (the staged epilogues use it).  EPI_F32 writes a stream-K
+  // partial tile to f32_slot when it is set, else the split's partial rows.
+  float* f32_slot = nullptr;
   auto epilogue = [&](const int64_t m0, const int64_t n0, char* stage) __attribute__((always_inline)) {
     if constexpr (Cfg::SWAP) {
       // Accumulator 4b+q of lane l is C[row l%32][col 8b + 4h + q] of its 32x32
       // block (h = l / 32).  N is a multiple of 8, so each 8-column (bf16) or
       // 4-column (fp32) piece is wholly inside or outside the matrix.
-  #pragma unroll
+#pragma unroll
       for (int i = 0; i < FM; ++i)
-  #pragma unroll
+#pragma unroll
         for (int j = 0; j < FN; ++j) {
           const int64_t row = m0 + wm * TM + i * 32 + lrow;
           const int64_t colb = n0 + wn * TN + j * 32;
@@ -582,15 +590,15 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             // pk[b]: columns 8b+4h .. +3 as two bf16 pairs.  One permlane32 swap
             // per dword gives lane half 0 columns 0..15 and half 1 columns 16..31.
             uint32_t pk[4][2];
-  #pragma unroll
+#pragma unroll
             for (int b = 0; b < 4; ++b)
-  #pragma unroll
+#pragma unroll
               for (int e = 0; e < 2; ++e)
                 pk[b][e] = bf16x2_rne(acc[i][j][4 * b + 2 * e], acc[i][j][4 * b + 2 * e + 1]);
             uint32_t out[2][4];
-  #pragma unroll
+#pragma unroll
             for (int c = 0; c < 2; ++c)
-  #pragma unroll
+#pragma unroll
               for (int e = 0; e < 2; ++e) {
                 const auto sw = __builtin_amdgcn_permlane32_swap(pk[c][e], pk[c + 2][e], false, false);
                 out[c][e] = sw[0];       // half 0: columns 8c + 2e ..; half 1: 16 + 8c + 2e ..
@@ -599,14 +607,21 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             const int64_t col = colb + 16 * lhalf;
             if (row < g.M) {
               __bf16* dst = (__bf16*)g.C + row * g.ldc + col;
-  #pragma unroll
+#pragma unroll
               for (int c = 0; c < 2; ++c)
                 if (col + 8 * c < g.N) *(uint4*)(dst + 8 * c) = make_uint4(out[c][0], out[c][1], out[c][2], out[c][3]);
             }
+          } else if (f32_slot != nullptr) {
+            // stream-K partial: the whole tile, tile-local rows and columns
+            float* dst = f32_slot + (row - m0) * BN + (colb - n0);
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+              *(float4*)(dst + 8 * b + 4 * lhalf) =
+                  make_float4(acc[i][j][4 * b], acc[i][j][4 * b + 1], acc[i][j][4 * b + 2], acc[i][j][4 * b + 3]);
           } else {
             float* part = (float*)g.C + (int64_t)blockIdx.y * g.M * g.N;
             if (row < g.M) {
-  #pragma unroll
+#pragma unroll
               for (int b = 0; b < 4; ++b) {
                 const int64_t col = colb + 8 * b + 4 * lhalf;
                 if (col < g.N)
@@ -638,18 +653,18 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       // lane are features 8b + 4h + 0..3 of token column l % 32.  Lanes l and
       // l+32 exchange halves so that each writes 16 contiguous features
       // (half 0: 0..15, half 1: 16..31 of the 32-row block) of its token row.
-  #pragma unroll
+#pragma unroll
       for (int i = 0; i < FM; ++i)
-  #pragma unroll
+#pragma unroll
         for (int j = 0; j < FN; ++j) {
           const int64_t t = n0 + wn * TN + j * 32 + lrow;
           const int64_t f32 = m0 + wm * TM + i * 32;
           uint2 mine[4];   // block b: features f32 + 8b + 4h .. +3 as 4 bf16
           if constexpr (Cfg::EPI == EPI_ACT_DENSE) {
-  #pragma unroll
+#pragma unroll
             for (int b = 0; b < 4; ++b) {
               uint32_t v[2];
-  #pragma unroll
+#pragma unroll
               for (int e = 0; e < 2; ++e) {
                 // h rounded to bf16 (RNE), relu'd, squared (act_square) and rounded
                 const uint32_t r = relu_bits2(bf16x2_rne(acc[i][j][4 * b + 2 * e], acc[i][j][4 * b + 2 * e + 1]));
@@ -663,13 +678,13 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
               mine[b] = make_uint2(v[0], v[1]);
             }
           } else {
-  #pragma unroll
+#pragma unroll
             for (int b = 0; b < 4; ++b) {
               const int64_t f = f32 + 8 * b + 4 * lhalf;
               uint2 a = make_uint2(0u, 0u);
               if (t < g.N && f < g.f_valid) a = *(const uint2*)(g.act + t * g.ld_act + f);
               uint32_t v[2];
-  #pragma unroll
+#pragma unroll
               for (int e = 0; e < 2; ++e) {
                 const uint32_t w = e ? a.y : a.x;
                 float x0 = __builtin_bit_cast(float, w << 16), x1 = __builtin_bit_cast(float, w & 0xFFFF0000u);
@@ -687,7 +702,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           // swapping (block 0, block 2) and (block 1, block 3) across the halves
           // leaves each lane two runs of 8 consecutive features.
           uint32_t lo[4], hi[4];
-  #pragma unroll
+#pragma unroll
           for (int e = 0; e < 2; ++e) {
             const auto s0 = __builtin_amdgcn_permlane32_swap(e ? mine[0].y : mine[0].x, e ? mine[2].y : mine[2].x,
                                                              false, false);
@@ -732,7 +747,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       if constexpr (Cfg::EPI == EPI_DH) {
         // stored S rows of this tile -> LDS
         constexpr int VCH = BN * (BM / 16);               // 16-byte value chunks
-  #pragma unroll
+#pragma unroll
         for (int it = 0; it < VCH / NT; ++it) {
           const int q = it * NT + tid, row = q / (BM / 16), c = q % (BM / 16);
           if (row < t_end && c * 16 < f_end) {
@@ -742,7 +757,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           }
         }
         constexpr int MCH = BN * (BM / 64);               // 8-byte metadata chunks
-  #pragma unroll
+#pragma unroll
         for (int it = 0; it < (MCH + NT - 1) / NT; ++it) {
           const int q = it * NT + tid, row = q / (BM / 64), c = q % (BM / 64);
           if (q < MCH && row < t_end && c * 64 < f_end) {
@@ -753,10 +768,9 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         }
         __syncthreads();
       }
-
-  #pragma unroll
+#pragma unroll
       for (int i = 0; i < FM; ++i)
-  #pragma unroll
+#pragma unroll
         for (int j = 0; j < FN; ++j) {
           const int tl = wn * TN + j * 32 + lrow;         // token within the tile
           const int fl = wm * TM + i * 32;                // first feature of the 32-row block
@@ -764,7 +778,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           uint32_t pair[4], codes = 0;
           if constexpr (Cfg::EPI == EPI_SPARSIFY) {
             uint32_t codes = 0;   // code of group b at bits 8b .. 8b+3
-  #pragma unroll
+#pragma unroll
             for (int b = 0; b < 4; ++b) {
               // h rounded to bf16 (RNE), relu'd, ranked (ties to the lower index)
               const uint32_t p01 = relu_bits2(bf16x2_rne(acc[i][j][4 * b], acc[i][j][4 * b + 1]));
@@ -779,7 +793,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             // 2b+1 (half 1) << 4; the swap hands half 0 its partner's codes
             const uint32_t other_codes = __builtin_amdgcn_permlane32_swap(codes, codes, false, false)[1];
             if (ok) {
-  #pragma unroll
+#pragma unroll
               for (int b = 0; b < 4; ++b)
                 *(uint32_t*)(lv + val_word(tl, fl / 4 + 2 * b + lhalf)) = pair[b];
               if (lhalf == 0) *(uint32_t*)(lm + tl * MP + fl / 8) = codes | (other_codes << 4);
@@ -789,14 +803,14 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             // 2 relu(h), relu(h) = bf16(sqrt(s)) exactly; result in place.
             if (ok) {
               const uint32_t word = *(const uint32_t*)(lm + tl * MP + fl / 8);
-  #pragma unroll
+#pragma unroll
               for (int b = 0; b < 4; ++b) {
                 uint32_t* loc = (uint32_t*)(lv + val_word(tl, fl / 4 + 2 * b + lhalf));
                 const uint32_t sv = *loc;
                 const uint32_t code = (word >> (8 * b + 4 * lhalf)) & 0xFu;
                 const uint32_t i0 = code & 3u, i1 = code >> 2;
                 float ds[4];
-  #pragma unroll
+#pragma unroll
                 for (int q = 0; q < 4; ++q) ds[q] = acc[i][j][4 * b + q];
                 const float d0 = i0 == 0u ? ds[0] : i0 == 1u ? ds[1] : ds[2];
                 const float d1 = i1 == 1u ? ds[1] : i1 == 2u ? ds[2] : ds[3];
@@ -815,7 +829,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       // LDS -> global: whole 16-byte pieces of each token row
       uint16_t* dst = Cfg::EPI == EPI_SPARSIFY ? g.sv : g.dv;
       constexpr int VCH = BN * (BM / 16);
-  #pragma unroll
+#pragma unroll
       for (int it = 0; it < VCH / NT; ++it) {
         const int q = it * NT + tid, row = q / (BM / 16), c = q % (BM / 16);
         if (row < t_end && c * 16 < f_end) {
@@ -825,7 +839,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       }
       if constexpr (Cfg::EPI == EPI_SPARSIFY) {
         constexpr int MCH = BN * (BM / 64);
-  #pragma unroll
+#pragma unroll
         for (int it = 0; it < (MCH + NT - 1) / NT; ++it) {
           const int q = it * NT + tid, row = q / (BM / 64), c = q % (BM / 64);
           if (q < MCH && row < t_end && c * 64 < f_end) {
@@ -946,53 +960,74 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       s_in = ns_in;
     }
   } else {
-    // A: the 2:4 K-major operand, expanded in registers; B: DMA.  One tile
-    // per workgroup.  The next step's A loads and B DMA are issued before the
-    // current step's MFMAs; A is written to LDS after them; one barrier per
-    // step.
-    int64_t m0, n0;
-    origin(xcd_remap(blockIdx.x, ntiles), m0, n0);
-    zero_acc();
-    StagerKMSP<BM, NT> sa;
+    // A: the 2:4 K-major operand, expanded in registers; B: DMA.  The next
+    // step's A loads and B DMA are issued before the current step's MFMAs; A
+    // is written to LDS after them; one barrier per step.
     using TB = std::conditional_t<Cfg::B_KM, DmaTileKM<BN, NW>, DmaTile<BN, Cfg::B_ROWB, false, NW>>;
     const uint32_t smem_lds = lds_u32(smem);
     uint32_t offB[TB::PER_WAVE];
 #pragma unroll
     for (int j = 0; j < TB::PER_WAVE; ++j) offB[j] = TB::lane_off(j, g.ldb, wave, lane);
-    int b_steps_in = 0;   // steps whose B loads need no bounds checks
-    if (n0 + BN <= g.N) {
-      const int64_t k_in = g.kb_valid - kbeg;
-      b_steps_in = k_in <= 0 ? 0 : (int)(k_in / BK < nsteps ? k_in / BK : nsteps);
-    }
-    b_steps_in = __builtin_amdgcn_readfirstlane(b_steps_in);
-    auto issue_b = [&](int step) __attribute__((always_inline)) {
-      const int64_t k0 = kbeg + (int64_t)step * BK;
-      const uint32_t base = smem_lds + (uint32_t)((step & 1) * Cfg::STAGE) + Cfg::A_BYTES;
-      if (step < b_steps_in)
-        TB::template issue_fast<0, TB::PER_WAVE>(TB::step_base(g.B, g.ldb, n0, k0), offB, base, wave);
-      else
-        TB::template issue<0, TB::PER_WAVE>(g.B, g.ldb, n0, g.N, k0, g.kb_valid, base, wave, lane);
-    };
-    if (nsteps > 0) {
-      sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, kbeg, g.ka_valid, tid);
-      issue_b(0);
-      sa.store(smem, tid);
-      wait_vmcnt<0>();
-      __syncthreads();
-    }
-    for (int s = 0; s < nsteps; ++s) {
-      const int buf = s & 1;
-      const bool more = s + 1 < nsteps;
-      if (more) {
-        sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, kbeg + (int64_t)(s + 1) * BK, g.ka_valid, tid);
-        issue_b(s + 1);
+    // Accumulate steps [0, ns) of the K range starting at kb of the tile at (m0, n0).
+    auto run_tile = [&](int64_t m0, int64_t n0, int64_t kb, int ns) __attribute__((always_inline)) {
+      zero_acc();
+      StagerKMSP<BM, NT> sa;
+      int b_steps_in = 0;   // steps whose B loads need no bounds checks
+      if (n0 + BN <= g.N) {
+        const int64_t k_in = g.kb_valid - kb;
+        b_steps_in = k_in <= 0 ? 0 : (int)(k_in / BK < ns ? k_in / BK : ns);
       }
-      compute(smem + buf * Cfg::STAGE, [](int) {});
-      if (more) sa.store(smem + (buf ^ 1) * Cfg::STAGE, tid);
-      wait_vmcnt<0>();   // B's DMA of step s+1 has landed
-      __syncthreads();   // A's LDS writes and B's DMA of step s+1 are complete
+      b_steps_in = __builtin_amdgcn_readfirstlane(b_steps_in);
+      auto issue_b = [&](int step) __attribute__((always_inline)) {
+        const int64_t k0 = kb + (int64_t)step * BK;
+        const uint32_t base = smem_lds + (uint32_t)((step & 1) * Cfg::STAGE) + Cfg::A_BYTES;
+        if (step < b_steps_in)
+          TB::template issue_fast<0, TB::PER_WAVE>(TB::step_base(g.B, g.ldb, n0, k0), offB, base, wave);
+        else
+          TB::template issue<0, TB::PER_WAVE>(g.B, g.ldb, n0, g.N, k0, g.kb_valid, base, wave, lane);
+      };
+      if (ns > 0) {
+        sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, kb, g.ka_valid, tid);
+        issue_b(0);
+        sa.store(smem, tid);
+        wait_vmcnt<0>();
+        __syncthreads();
+      }
+      for (int s = 0; s < ns; ++s) {
+        const int buf = s & 1;
+        const bool more = s + 1 < ns;
+        if (more) {
+          sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, kb + (int64_t)(s + 1) * BK, g.ka_valid, tid);
+          issue_b(s + 1);
+        }
+        compute(smem + buf * Cfg::STAGE, [](int) {});
+        if (more) sa.store(smem + (buf ^ 1) * Cfg::STAGE, tid);
+        wait_vmcnt<0>();   // B's DMA of step s+1 has landed
+        __syncthreads();   // A's LDS writes and B's DMA of step s+1 are complete
+      }
+    };
+    int64_t m0, n0;
+    if (g.stream_steps > 0) {
+      // Stream-K: this workgroup's share [beg, end) of the tiles x S steps,
+      // one partial tile per tile it touches.
+      const int64_t S = g.stream_steps, I = (int64_t)ntiles * S;
+      const int64_t beg = (int64_t)blockIdx.x * I / gridDim.x, end = (int64_t)(blockIdx.x + 1) * I / gridDim.x;
+      const int64_t t_first = beg / S;
+      for (int64_t it = beg; it < end;) {
+        const int t = (int)(it / S);
+        const int64_t k_first = it - (int64_t)t * S;
+        const int64_t k_last = end - (int64_t)t * S < S ? end - (int64_t)t * S : S;
+        origin(t, m0, n0);
+        run_tile(m0, n0, k_first * BK, (int)(k_last - k_first));
+        f32_slot = (float*)g.C + ((int64_t)blockIdx.x * g.stream_segs + (t - t_first)) * (BM * BN);
+        epilogue(m0, n0, smem);
+        it = (int64_t)t * S + k_last;
+      }
+    } else {
+      origin(xcd_remap(blockIdx.x, ntiles), m0, n0);
+      run_tile(m0, n0, kbeg, nsteps);
+      epilogue(m0, n0, smem);
     }
-    epilogue(m0, n0, smem);
   }
 }
 
