@@ -167,13 +167,21 @@ hipError_t fill_zero(float* p, int64_t n, hipStream_t st) {
 // waves (two per SIMD) hide LDS and global latency better than four larger
 // wave tiles.
 // Dense products with both operands K-contiguous: 256 x BN tiles, 4 x 2 waves.
-template <int BN, int EPI, bool M_FAST>
-using CfgNT = GemmCfg<256, BN, 4, 2, OP_K, OP_K, EPI, M_FAST, 2>;
-// 2:4 sparse A (smfmac) times K-contiguous B: 256 x 128 tiles, 2 x 4 waves.
-using CfgSP = GemmCfg<256, 128, 2, 4, OP_SP, OP_K, EPI_BF16, false, 2>;
+template <int BN, int EPI, bool M_FAST, int DEEP = 0>
+using CfgNT = GemmCfg<256, BN, 4, 2, OP_K, OP_K, EPI, M_FAST, 2, true, false, 128, DEEP>;
+// Plain bf16 outputs (A = the token-major activation streaming from HBM, B =
+// a weight factor resident in L2): A gets three LDS stages, B two.
+using CfgNT3 = CfgNT<256, EPI_BF16, false, 1>;
+// 2:4 sparse A (smfmac) times K-contiguous B: 256 x 128 tiles, 4 x 2 waves
+// (64 x 64 per wave), 128 dense K per step, two LDS stages.  (Measured: 64-K
+// steps with three or four stages lose more to per-step overhead than the
+// deeper prefetch gains; 2 x 4 waves read more fragments per MFMA.)
+using CfgSP = GemmCfg<256, 128, 4, 2, OP_SP, OP_K, EPI_BF16, false, 2>;
 // Contraction over tokens (K = T): both operands stored [T x rows].
 // Both operands are K-major: the dense ones go to LDS by DMA, the 2:4 one is
 // expanded in registers; fragments are read with the transposing LDS read.
+// K = T weight-gradient products (both operands token-major and streaming;
+// a three-stage ring for one of them measured no gain).
 template <int AMODE>
 using CfgTT = GemmCfg<256, 256, 4, 2, AMODE, OP_T, EPI_F32, false>;
 
@@ -216,7 +224,7 @@ hipError_t gemm_nt_bf16(const char* tag, const uint16_t* A, int64_t lda, const u
   g.A = A; g.lda = lda; g.B = Bt; g.ldb = ldb; g.C = C; g.ldc = ldc;
   g.M = M; g.N = N; g.K = K; g.m_valid = M; g.ka_valid = K; g.kb_valid = K;
   if (N <= 128) return launch<CfgNT<128, EPI_BF16, false>>(tag, g, 1, st);
-  return launch<CfgNT<256, EPI_BF16, false>>(tag, g, 1, st);
+  return launch<CfgNT3>(tag, g, 1, st);
 }
 
 // Work split of a K = T product.  Split-K: enough workgroups to cover the 256
@@ -410,7 +418,7 @@ hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
     g.A = w.V_upT; g.lda = r; g.B = a.P; g.ldb = r;
     g.M = Fp; g.N = T; g.K = r; g.m_valid = Fp; g.ka_valid = r; g.kb_valid = r;
     g.act = a.s_vals; g.ld_act = F; g.f_valid = F; g.act_square = 1;
-    ELAS_TRY(launch<CfgNT<256, EPI_ACT_DENSE, true>>("k2_up_relu2_dense", g, 1, st));
+    ELAS_TRY(launch<CfgNT<256, EPI_ACT_DENSE, true, 2>>("k2_up_relu2_dense", g, 1, st));
     ELAS_TRY(gemm_nt_bf16("k3_down_gemm_dense", a.s_vals, F, w.U_downT, Fp, a.Z, r, T, r, F, st));
   }
   // Y = Z V_down
@@ -465,7 +473,7 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
       h.A = w.V_upT; h.lda = r; h.B = a.P_in; h.ldb = r;
       h.M = Fp; h.N = T; h.K = r; h.m_valid = Fp; h.ka_valid = r; h.kb_valid = r;
       h.act = w.R; h.ld_act = F; h.f_valid = F; h.act_square = 0;
-      ELAS_TRY(launch<CfgNT<256, EPI_ACT_DENSE, true>>("b3_relu_h_recompute", h, 1, st));
+      ELAS_TRY(launch<CfgNT<256, EPI_ACT_DENSE, true, 2>>("b3_relu_h_recompute", h, 1, st));
       act = w.R;
       square = 0;
     }
@@ -473,7 +481,7 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
     g.A = a.U_down; g.lda = r; g.B = w.dZ; g.ldb = r;
     g.M = Fp; g.N = T; g.K = r; g.m_valid = F; g.ka_valid = r; g.kb_valid = r;
     g.act = const_cast<uint16_t*>(act); g.ld_act = F; g.f_valid = F; g.act_square = square; g.dact = w.dH;
-    ELAS_TRY(launch<CfgNT<256, EPI_DH_DENSE, true>>(a.ste ? "b3_dH_ste" : "b3_dH_dense", g, 1, st));
+    ELAS_TRY(launch<CfgNT<256, EPI_DH_DENSE, true, 2>>(a.ste ? "b3_dH_ste" : "b3_dH_dense", g, 1, st));
     if (a.dense) {
       // dU_down = S^T dZ with the dense S
       ELAS_TRY(gemm_tt_f32<OP_T>("b4_dU_down_dense", a.s_vals, F, nullptr, 0, w.dZ, r, F, r, T, w.part, a.dU_down, F,

@@ -97,11 +97,18 @@ struct GemmArgs {
 };
 
 template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int AMODE_, int BMODE_, int EPI_, bool M_FAST_,
-          int STAGES_ = 2, bool PIPE_ = true>
+          int STAGES_ = 2, bool PIPE_ = true, bool PIN_ = false, int SPK_ = 128, int DEEP_ = 0>
 struct GemmCfg {
+  // DEEP: separate LDS rings with three stages (prefetched two steps ahead)
+  // for one operand, 1 = A or 2 = B, the one streaming from HBM, and two
+  // (one step ahead) for the other.  Plain-output epilogues only.
+  static constexpr int DEEP = DEEP_;
   // PIPE: double-buffer the MFMA fragments (read sub-step kk+1 during kk's
   // MFMAs); off saves registers.
   static constexpr bool PIPE = PIPE_;
+  // PIN: fence the scheduler around each sub-step's MFMAs, so that the reads
+  // of the next sub-step are issued ahead of them as written (costs registers).
+  static constexpr bool PIN = PIN_;
   static constexpr int BM = BM_, BN = BN_, WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
   static constexpr int NW = WAVES_M_ * WAVES_N_, NT = 64 * NW;
   static constexpr int AMODE = AMODE_, BMODE = BMODE_, EPI = EPI_;
@@ -119,11 +126,15 @@ struct GemmCfg {
   // K-major operand, expanded in registers) A is register-staged.
   static constexpr bool DIRECT = AMODE_ != OP_TSP;
   static constexpr int STAGES = STAGES_;
-  static constexpr int BK = SPARSE ? 128 : 64;         // dense contraction per step
-  static constexpr int A_ROWB = 128;                     // bytes per LDS row of A (64 values)
-  static constexpr int B_ROWB = SPARSE ? 256 : 128;      // bytes per LDS row of B
+  // dense contraction per step: 64, or SPK (64 or 128) for a 2:4 operand
+  static constexpr int BK = SPARSE ? SPK_ : 64;
+  static_assert(SPK_ == 64 || SPK_ == 128, "2:4 K step");
+  static constexpr int KK = SPARSE ? BK / 32 : 4;       // MFMA sub-steps per step
+  static constexpr int A_ROWB = SPARSE ? BK : 128;       // bytes per LDS row of A (BK/2 kept or 64 dense values)
+  static constexpr int B_ROWB = SPARSE ? 2 * BK : 128;   // bytes per LDS row of B
+  static constexpr int M_ROWB = SPARSE ? BK / 8 : 0;     // metadata bytes per row
   static constexpr int A_BYTES = BM * A_ROWB;
-  static constexpr int AM_BYTES = SPARSE ? BM * 16 : 0;
+  static constexpr int AM_BYTES = BM * M_ROWB;
   static constexpr int B_BYTES = BN * B_ROWB;
   static constexpr int STAGE = A_BYTES + AM_BYTES + B_BYTES;
   static constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
@@ -132,13 +143,17 @@ struct GemmCfg {
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be a multiple of 32");
   static_assert(DIRECT || STAGES_ == 2, "register staging uses two LDS buffers");
   static_assert(!(A_KM || B_KM) || !SPARSE, "2:4 along K with a K-major partner is not used");
-  static_assert(STAGES_ == 2 || STAGES_ == 3, "2 or 3 stages");
+  static_assert(STAGES_ >= 2 && STAGES_ <= 4, "2 to 4 stages");
   // The compressed-activation epilogues stage a BN x BM/2 tile of kept values
   // in one stage buffer and the metadata rows (BM/8 bytes + 4 pad) after the
   // stages.
   static constexpr bool STAGED_EPI = EPI_ == EPI_SPARSIFY || EPI_ == EPI_DH;
   static constexpr int META_PITCH = BM_ / 8 + 4;
-  static constexpr int LDS_BYTES = STAGES_ * STAGE + (STAGED_EPI ? (BN_ * META_PITCH + 15) / 16 * 16 : 0);
+  static constexpr int A_PART = A_BYTES + AM_BYTES;   // one stage of A (and its metadata)
+  static constexpr int LDS_BYTES = DEEP_ == 1   ? 3 * A_PART + 2 * B_BYTES
+                                   : DEEP_ == 2 ? 2 * A_PART + 3 * B_BYTES
+                                                : STAGES_ * STAGE + (STAGED_EPI ? (BN_ * META_PITCH + 15) / 16 * 16 : 0);
+  static_assert(DEEP_ == 0 || (STAGES_ == 2 && !STAGED_EPI && DIRECT), "three-stage ring: plain epilogues, direct staging");
   static_assert(!STAGED_EPI || (BM_ == 256 && BN_ * BM_ <= STAGE && DIRECT), "staged epilogue layout");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 };
@@ -148,6 +163,24 @@ struct GemmCfg {
 // the chunk with (row ^ row/8) & 7 spreads both patterns over 8 different
 // 16-byte bank groups.
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row ^ (row >> 3)) & 7); }
+// 256-byte rows (the dense operand of a 2:4 product, 128 K per step): 16
+// chunks per row; XOR-ing with row % 16 gives the 16 rows that one 16-lane
+// group of a fragment read touches 16 different chunk positions.
+__device__ __forceinline__ int swz16(int row, int chunk) { return chunk ^ (row & 15); }
+// 64-byte rows (kept values of a 2:4 operand, 64 K per step): four rows share
+// a 256-byte bank cycle, so the chunk is XOR-ed with (row / 4) % 4 to give 16
+// consecutive rows 16 different 16-byte positions.
+__device__ __forceinline__ int swz4(int row, int chunk) { return chunk ^ ((row >> 2) & 3); }
+template <int ROWB>
+__device__ __forceinline__ int swz_row(int row, int chunk) {
+  static_assert(ROWB == 64 || ROWB == 128 || ROWB == 256, "row size");
+  if constexpr (ROWB == 64)
+    return swz4(row, chunk);
+  else if constexpr (ROWB == 128)
+    return swz(row, chunk);
+  else
+    return swz16(row, chunk);
+}
 
 // Expand 2 groups (4 kept values in 8 bytes + 2 codes in one byte) to 8 dense
 // bf16 values packed as a uint4.
@@ -197,14 +230,19 @@ __device__ __forceinline__ const void* uniform_ptr(const void* p) {
   const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
   return (const void*)(uintptr_t)(((uint64_t)hi << 32) | lo);
 }
+__device__ __forceinline__ int64_t uniform_i64(int64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
 __device__ __forceinline__ void dma_b128_s(const void* sbase, uint32_t voff, uint32_t lds_wave_base) {
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(uniform_ptr(sbase)),
-               "s"(lds_wave_base)
+               "s"(__builtin_amdgcn_readfirstlane(lds_wave_base))
                : "memory", "m0");
 }
 __device__ __forceinline__ void dma_b32_s(const void* sbase, uint32_t voff, uint32_t lds_wave_base) {
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(voff), "s"(uniform_ptr(sbase)),
-               "s"(lds_wave_base)
+               "s"(__builtin_amdgcn_readfirstlane(lds_wave_base))
                : "memory", "m0");
 }
 template <int N>
@@ -237,7 +275,7 @@ struct DmaTile {
       const int blk = wave * PER_WAVE + j;
       const int off = blk * 1024 + lane * 16;
       const int row = off / ROWB, pos = (off % ROWB) / 16;
-      const int c = swz(row, pos);           // swz is an involution in the chunk index
+      const int c = swz_row<ROWB>(row, pos);   // the swizzle is an involution in the chunk index
       const int64_t grow = row0 + row, gk = k0 + (int64_t)c * KPC;
       const void* src = (grow < rows_valid && gk < k_valid) ? (const void*)(p + grow * ld + (KEPT ? gk / 2 : gk))
                                                            : (const void*)g_dma_zero;
@@ -252,7 +290,7 @@ struct DmaTile {
     const int blk = wave * PER_WAVE + j;
     const int off = blk * 1024 + lane * 16;
     const int row = off / ROWB, pos = (off % ROWB) / 16;
-    return (uint32_t)row * (uint32_t)(ld * 2) + (uint32_t)swz(row, pos) * 16u;
+    return (uint32_t)row * (uint32_t)(ld * 2) + (uint32_t)swz_row<ROWB>(row, pos) * 16u;
   }
   __device__ __forceinline__ static const char* step_base(const uint16_t* p, int64_t ld, int64_t row0, int64_t k0) {
     return (const char*)(p + row0 * ld + (KEPT ? k0 / 2 : k0));
@@ -264,11 +302,11 @@ struct DmaTile {
   }
 };
 
-// Metadata of a 2:4 tile: ROWS rows x 16 bytes (128 dense K), dword DMA
-// (256 bytes = 16 rows per wave instruction).
-template <int ROWS, int NW>
+// Metadata of a 2:4 tile: ROWS rows x MROWB bytes (8 MROWB dense K), dword
+// DMA (256 bytes per wave instruction).
+template <int ROWS, int MROWB, int NW>
 struct DmaMeta {
-  static constexpr int BLOCKS = ROWS * 16 / 256;
+  static constexpr int BLOCKS = ROWS * MROWB / 256;
   static constexpr int PER_WAVE = BLOCKS / NW;
   static_assert(BLOCKS % NW == 0, "meta blocks per wave");
   template <int J0, int J1>
@@ -279,7 +317,7 @@ struct DmaMeta {
     for (int j = J0; j < J1; ++j) {
       const int blk = wave * PER_WAVE + j;
       const int off = blk * 256 + lane * 4;
-      const int row = off / 16, dw = (off % 16) / 4;     // dword dw covers dense K 32 dw .. 32 dw + 31
+      const int row = off / MROWB, dw = (off % MROWB) / 4;   // dword dw covers dense K 32 dw .. 32 dw + 31
       const int64_t grow = row0 + row;
       const void* src = (grow < rows_valid && k0 + 32 * (dw + 1) <= k_valid)
                             ? (const void*)(pm + grow * ldm + k0 / 8 + dw * 4)
@@ -290,7 +328,7 @@ struct DmaMeta {
   __device__ __forceinline__ static uint32_t lane_off(int j, int64_t ldm, int wave, int lane) {
     const int blk = wave * PER_WAVE + j;
     const int off = blk * 256 + lane * 4;
-    return (uint32_t)(off / 16) * (uint32_t)ldm + (uint32_t)(off % 16);
+    return (uint32_t)(off / MROWB) * (uint32_t)ldm + (uint32_t)(off % MROWB);
   }
   __device__ __forceinline__ static const char* step_base(const uint8_t* pm, int64_t ldm, int64_t row0, int64_t k0) {
     return (const char*)(pm + row0 * ldm + k0 / 8);
@@ -306,18 +344,19 @@ struct DmaMeta {
 // A K-major operand (stored [K x rows], rows contiguous) is staged as it is:
 // LDS row k (one per contraction index of the step, 64 of them) holds the
 // tile's ROWS elements, in 32-byte chunks of 16 elements; chunk c of row k
-// sits at chunk position c ^ (k & 3).
+// sits at chunk position c ^ 2 (k & 3).
 //
 // ds_read_b64_tr_b16 (gfx950, pinned by a probe): within each group of 16
 // lanes, lane j reads 4 consecutive 16-bit elements; lane i of the group then
 // receives element i % 4 of lane 4q + i/4's read, for q = 0..3.  When lane j
 // reads row k0 + j/4 at columns c0 + 4 (j % 4), lane i therefore receives
-// column c0 + i of rows k0..k0+3: one MFMA fragment half.  The 16 lanes touch
-// rows k0..k0+3 at one logical chunk, which the swizzle spreads over four
-// bank groups.
+// column c0 + i of rows k0..k0+3: one MFMA fragment half.  The 32 lanes
+// served together touch rows k0..k0+3 at two adjacent logical chunks (c even,
+// c + 1); the swizzle spreads these eight 32-byte pieces over eight distinct
+// positions, i.e. all 64 banks (each row is a multiple of 256 bytes).
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ int km_swz(int k, int chunk) { return chunk ^ (k & 3); }
+__device__ __forceinline__ int km_swz(int k, int chunk) { return chunk ^ ((k & 3) << 1); }
 
 // Fragment of a v_mfma_f32_32x32x16_bf16 operand from a K-major LDS tile:
 // lane l gets columns col0 + l % 32, contraction indices 16 kk + 8 (l / 32) + 0..7.
@@ -483,10 +522,8 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
   // kk+1 are read while sub-step kk's MFMAs run; hook(kk) runs between the
   // reads and the MFMAs of sub-step kk (it issues part of the next stage's
   // loads in the direct path).
-  auto compute = [&](const char* base, auto&& hook) __attribute__((always_inline)) {
-    const char* lA = base;
+  auto compute = [&](const char* lA, const char* lB, auto&& hook) __attribute__((always_inline)) {
     const char* lM = lA + Cfg::A_BYTES;
-    const char* lB = lM + Cfg::AM_BYTES;
     if constexpr (!SPARSE) {
       bf16x8 af[2][FM], bfr[2][FN];
       auto read = [&](int kk, int slot) __attribute__((always_inline)) {
@@ -519,19 +556,30 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           read(kk, 0);
         }
         hook(kk);
+        // keep the reads of sub-step kk+1 ahead of this sub-step's MFMAs (the
+        // scheduler would otherwise sink each read next to its consumer)
+        if constexpr (Cfg::PIN) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
           for (int j = 0; j < FN; ++j)
             acc[i][j] = Cfg::SWAP ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0)
                                   : __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
+        if constexpr (Cfg::PIN) __builtin_amdgcn_sched_barrier(0);
       }
     } else {
-      uint4 meta[FM];
+      constexpr int KK = Cfg::KK;
+      uint32_t meta[FM][KK];   // metadata word of sub-step kk (32 dense K) of each row block
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
         const int row = wm * TM + i * 32 + lrow;
-        meta[i] = *(const uint4*)(lM + row * 16);
+        if constexpr (KK == 4) {
+          const uint4 w = *(const uint4*)(lM + row * 16);
+          meta[i][0] = w.x; meta[i][1] = w.y; meta[i][2] = w.z; meta[i][3] = w.w;
+        } else {
+          const uint2 w = *(const uint2*)(lM + row * 8);
+          meta[i][0] = w.x; meta[i][1] = w.y;
+        }
       }
       bf16x8 af[2][FM];
       bf16x16 bfr[2][FN];
@@ -539,33 +587,33 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
           const int row = wm * TM + i * 32 + lrow;
-          af[slot][i] = *(const bf16x8*)(lA + row * 128 + swz(row, 2 * kk + lhalf) * 16);
+          af[slot][i] = *(const bf16x8*)(lA + row * Cfg::A_ROWB + swz_row<Cfg::A_ROWB>(row, 2 * kk + lhalf) * 16);
         }
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
           const int row = wn * TN + j * 32 + lrow;
-          const bf16x8 lo = *(const bf16x8*)(lB + row * 256 + swz(row, 4 * kk + lhalf) * 16);
-          const bf16x8 hi = *(const bf16x8*)(lB + row * 256 + swz(row, 4 * kk + 2 + lhalf) * 16);
+          constexpr int RB = Cfg::B_ROWB;
+          const bf16x8 lo = *(const bf16x8*)(lB + row * RB + swz_row<RB>(row, 4 * kk + lhalf) * 16);
+          const bf16x8 hi = *(const bf16x8*)(lB + row * RB + swz_row<RB>(row, 4 * kk + 2 + lhalf) * 16);
           bfr[slot][j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
         }
       };
       read(0, 0);
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {       // four 32-wide smfmac steps per 128-wide K step
+      for (int kk = 0; kk < KK; ++kk) {      // 32-wide smfmac sub-steps
         const int cur = kk & 1;
-        if (kk + 1 < 4) read(kk + 1, cur ^ 1);
+        if (kk + 1 < KK) read(kk + 1, cur ^ 1);
         hook(kk);
         int idx[FM];
 #pragma unroll
-        for (int i = 0; i < FM; ++i) {
-          const uint32_t w = kk == 0 ? meta[i].x : kk == 1 ? meta[i].y : kk == 2 ? meta[i].z : meta[i].w;
-          idx[i] = (int)(w >> (16 * lhalf));
-        }
+        for (int i = 0; i < FM; ++i) idx[i] = (int)(meta[i][kk] >> (16 * lhalf));
+        if constexpr (Cfg::PIN) __builtin_amdgcn_sched_barrier(0);   // reads of kk+1 stay ahead of these MFMAs
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
           for (int j = 0; j < FN; ++j)
             acc[i][j] = __builtin_amdgcn_smfmac_f32_32x32x32_bf16(af[cur][i], bfr[cur][j], acc[i][j], idx[i], 0, 0);
+        if constexpr (Cfg::PIN) __builtin_amdgcn_sched_barrier(0);
       }
     }
   };
@@ -854,7 +902,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
   if constexpr (Cfg::DIRECT) {
     using TA = std::conditional_t<Cfg::A_KM, DmaTileKM<BM, NW>, DmaTile<BM, Cfg::A_ROWB, SPARSE, NW>>;
     using TB = std::conditional_t<Cfg::B_KM, DmaTileKM<BN, NW>, DmaTile<BN, Cfg::B_ROWB, false, NW>>;
-    using TMeta = DmaMeta<BM, (SPARSE ? NW : 1)>;
+    using TMeta = DmaMeta<BM, (SPARSE ? Cfg::M_ROWB : 256), (SPARSE ? NW : 1)>;
     constexpr int LA = TA::PER_WAVE, LB = TB::PER_WAVE, LM = SPARSE ? TMeta::PER_WAVE : 0;
     constexpr int LOADS = LA + LB + LM;   // DMA instructions per wave per step
     const uint32_t smem_lds = lds_u32(smem);
@@ -879,85 +927,169 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       }
       return __builtin_amdgcn_readfirstlane(r);
     };
-    // Issue this wave's loads of step `step` of the tile at (m0, n0) into
-    // LDS stage `stage`.
-    auto issue = [&](int64_t m0, int64_t n0, int s_in, int step, int stage) __attribute__((always_inline)) {
+    // Issue this wave's loads of step `step` of the tile at (m0, n0): the A
+    // part (with its metadata) at LDS byte offset a_off, the B part at b_off.
+    // The checked path (edge tiles, tail steps) passes k0 and the lane index
+    // through an empty asm so that its addresses are formed afresh rather
+    // than kept in loop-carried registers across the main loop.
+    auto issue_a = [&](int64_t m0, int s_in, int step, uint32_t a_off) __attribute__((always_inline)) {
       const int64_t k0 = kbeg + (int64_t)step * BK;
-      const uint32_t base = smem_lds + (uint32_t)(stage * Cfg::STAGE);
-      const uint32_t base_b = base + Cfg::A_BYTES + Cfg::AM_BYTES;
+      const uint32_t base = smem_lds + a_off;
       if (step < s_in) {
         TA::template issue_fast<0, LA>(TA::step_base(g.A, g.lda, m0, k0), offA, base, wave);
         if constexpr (SPARSE)
           TMeta::template issue_fast<0, LM>(TMeta::step_base(g.Am, g.ldam, m0, k0), offM, base + Cfg::A_BYTES, wave);
-        TB::template issue_fast<0, LB>(TB::step_base(g.B, g.ldb, n0, k0), offB, base_b, wave);
       } else {
-        // Checked path (edge tiles, tail steps).  k0 and the lane index pass
-        // through an empty asm so that its addresses are formed afresh here
-        // rather than kept in loop-carried registers across the main loop.
-        int64_t kc = k0;
+        int64_t kc = uniform_i64(k0);
         int lc = lane;
         asm volatile("" : "+s"(kc), "+v"(lc));
         TA::template issue<0, LA>(g.A, g.lda, m0, g.m_valid, kc, g.ka_valid, base, wave, lc);
         if constexpr (SPARSE)
           TMeta::template issue<0, LM>(g.Am, g.ldam, m0, g.m_valid, kc, g.ka_valid, base + Cfg::A_BYTES, wave, lc);
-        TB::template issue<0, LB>(g.B, g.ldb, n0, g.N, kc, g.kb_valid, base_b, wave, lc);
+      }
+    };
+    auto issue_b = [&](int64_t n0, int s_in, int step, uint32_t b_off) __attribute__((always_inline)) {
+      const int64_t k0 = kbeg + (int64_t)step * BK;
+      const uint32_t base = smem_lds + b_off;
+      if (step < s_in) {
+        TB::template issue_fast<0, LB>(TB::step_base(g.B, g.ldb, n0, k0), offB, base, wave);
+      } else {
+        int64_t kc = uniform_i64(k0);
+        int lc = lane;
+        asm volatile("" : "+s"(kc), "+v"(lc));
+        TB::template issue<0, LB>(g.B, g.ldb, n0, g.N, kc, g.kb_valid, base, wave, lc);
       }
     };
 
     // Persistent schedule: this workgroup runs tiles first, first + stride,
     // ... (< end).  Steps are numbered across its tiles (gs = number of the
-    // current tile's step 0) and use stage (gs + s) % STAGES; the loads
-    // STAGES - 1 steps ahead run on into the next tile, so its first loads
-    // are in flight during this tile's last steps and epilogue.
+    // current tile's step 0); the loads issued ahead run on into the next
+    // tile, so its first loads are in flight during this tile's last steps
+    // and epilogue.
     const TileRange tr = tile_range(blockIdx.x, gridDim.x, ntiles);
     if (tr.first >= tr.end) return;
     int tile = tr.first;
     int64_t m0, n0;
     origin(tile, m0, n0);
     int s_in = steps_in_of(m0, n0);
-#pragma unroll
-    for (int p = 0; p < STAGES - 1; ++p)
-      if (p < nsteps) issue(m0, n0, s_in, p, p);
     int gs = 0;
-    for (;;) {
-      const int next = tile + tr.stride;
-      const bool has_next = next < tr.end;
-      int64_t nm0 = 0, nn0 = 0;
-      int ns_in = 0;
+    int next = tile + tr.stride;
+    bool has_next = next < tr.end;
+    int64_t nm0 = 0, nn0 = 0;
+    int ns_in = 0;
+    auto load_next = [&]() __attribute__((always_inline)) {
+      nm0 = 0; nn0 = 0; ns_in = 0;
       if (has_next) {
         origin(next, nm0, nn0);
         ns_in = steps_in_of(nm0, nn0);
       }
-      zero_acc();
-      for (int s = 0; s < nsteps; ++s) {
-        // wait for this wave's loads of step s.  At a tile's first step the
-        // previous epilogue's stores are outstanding too: wait for all.  With
-        // three stages the loads of step s + 1 (issued after those of s) may
-        // stay in flight.
-        if constexpr (STAGES == 3) {
-          if (s > 0 && (s + 1 < nsteps || has_next))
+    };
+    load_next();
+    // Lookahead step x (relative to the current tile's step 0) lies in this
+    // tile (x < nsteps) or in the next one; issue its A / B part if it exists.
+    auto ahead_a = [&](int x, uint32_t a_off) __attribute__((always_inline)) {
+      const bool here = x < nsteps;
+      if (here || (has_next && x - nsteps < nsteps)) issue_a(here ? m0 : nm0, here ? s_in : ns_in, here ? x : x - nsteps, a_off);
+    };
+    auto ahead_b = [&](int x, uint32_t b_off) __attribute__((always_inline)) {
+      const bool here = x < nsteps;
+      if (here || (has_next && x - nsteps < nsteps)) issue_b(here ? n0 : nn0, here ? s_in : ns_in, here ? x : x - nsteps, b_off);
+    };
+    auto exists = [&](int x) __attribute__((always_inline)) { return x < nsteps || (has_next && x - nsteps < nsteps); };
+
+    if constexpr (Cfg::DEEP != 0) {
+      // The deep operand's stage of global step q is q % 3, the other's q % 2;
+      // A's ring comes first.  Step s issues the shallow operand's step s+1,
+      // then the deep one's step s+2.
+      constexpr bool DA = Cfg::DEEP == 1;
+      constexpr int LOADS_DEEP = DA ? LA + LM : LB;
+      constexpr int NA = DA ? 3 : 2;
+      auto a_off = [](int q) { return (uint32_t)((q % NA) * Cfg::A_PART); };
+      auto b_off = [](int q) { return (uint32_t)(NA * Cfg::A_PART + (q % (DA ? 2 : 3)) * Cfg::B_BYTES); };
+      // x: step relative to the current tile's step 0; q = gs + x
+      auto ahead_deep = [&](int x, int q) __attribute__((always_inline)) {
+        if constexpr (DA) ahead_a(x, a_off(q)); else ahead_b(x, b_off(q));
+      };
+      auto ahead_shallow = [&](int x, int q) __attribute__((always_inline)) {
+        if constexpr (DA) ahead_b(x, b_off(q)); else ahead_a(x, a_off(q));
+      };
+      ahead_deep(0, 0);
+      ahead_shallow(0, 0);
+      ahead_deep(1, 1);
+      for (;;) {
+        zero_acc();
+        for (int s = 0; s < nsteps; ++s) {
+          // Step s needs both operands' step s; the loads issued after the
+          // shallow operand's step s are the deep one's step s+1 (issued with
+          // it at step s-1).  At a tile's first step the previous epilogue's
+          // stores are outstanding too: wait for all.
+          if (s > 0 && exists(s + 1))
+            wait_vmcnt<LOADS_DEEP>();
+          else
+            wait_vmcnt<0>();
+          lds_barrier();   // every wave's loads of step s landed; step s-1's reads are done
+          ahead_shallow(s + 1, gs + s + 1);
+          ahead_deep(s + 2, gs + s + 2);
+          compute(smem + a_off(gs + s), smem + b_off(gs + s), [](int) {});
+        }
+        epilogue(m0, n0, smem);
+        if (!has_next) break;
+        gs += nsteps;
+        tile = next;
+        m0 = nm0;
+        n0 = nn0;
+        s_in = ns_in;
+        next = tile + tr.stride;
+        has_next = next < tr.end;
+        load_next();
+      }
+    } else {
+      // Stage (gs + s) % STAGES holds step s, A part then B part; step s
+      // issues the loads STAGES - 1 steps ahead.
+      auto st_off = [](int q) { return (uint32_t)((q % STAGES) * Cfg::STAGE); };
+#pragma unroll
+      for (int p = 0; p < STAGES - 1; ++p) {
+        ahead_a(p, st_off(p));
+        ahead_b(p, st_off(p) + Cfg::A_PART);
+      }
+      for (;;) {
+        zero_acc();
+        for (int s = 0; s < nsteps; ++s) {
+          // wait for this wave's loads of step s.  The loads of the up to
+          // STAGES - 2 later steps already issued (after those of s: memory
+          // operations complete in issue order) may stay in flight.  At a
+          // tile's first step the previous epilogue's stores are outstanding
+          // too: wait for all.
+          int ahead = 0;
+          if (s > 0) {
+#pragma unroll
+            for (int j = 1; j <= STAGES - 2; ++j) ahead += exists(s + j) ? 1 : 0;
+          }
+          if (STAGES >= 4 && ahead >= 2)
+            wait_vmcnt<2 * LOADS>();
+          else if (STAGES >= 3 && ahead >= 1)
             wait_vmcnt<LOADS>();
           else
             wait_vmcnt<0>();
-        } else {
-          wait_vmcnt<0>();
+          lds_barrier();   // every wave's loads of step s landed; step s-1's reads are done
+          const int la = s + STAGES - 1;
+          ahead_a(la, st_off(gs + la));
+          ahead_b(la, st_off(gs + la) + Cfg::A_PART);
+          const char* st = smem + st_off(gs + s);
+          compute(st, st + Cfg::A_PART, [](int) {});
         }
-        lds_barrier();   // every wave's loads of step s landed; step s-1's reads are done
-        // the loads STAGES - 1 steps ahead: of this tile, or of the next one
-        const int la = s + STAGES - 1;
-        const bool here = la < nsteps;
-        if (here || (has_next && la - nsteps < nsteps))
-          issue(here ? m0 : nm0, here ? n0 : nn0, here ? s_in : ns_in, here ? la : la - nsteps, (gs + la) % STAGES);
-        compute(smem + ((gs + s) % STAGES) * Cfg::STAGE, [](int) {});
+        const int last = nsteps > 0 ? (gs + nsteps - 1) % STAGES : 0;
+        epilogue(m0, n0, smem + last * Cfg::STAGE);
+        if (!has_next) break;
+        gs += nsteps;
+        tile = next;
+        m0 = nm0;
+        n0 = nn0;
+        s_in = ns_in;
+        next = tile + tr.stride;
+        has_next = next < tr.end;
+        load_next();
       }
-      const int last = nsteps > 0 ? (gs + nsteps - 1) % STAGES : 0;
-      epilogue(m0, n0, smem + last * Cfg::STAGE);
-      if (!has_next) break;
-      gs += nsteps;
-      tile = next;
-      m0 = nm0;
-      n0 = nn0;
-      s_in = ns_in;
     }
   } else {
     // A: the 2:4 K-major operand, expanded in registers; B: DMA.  The next
@@ -1000,7 +1132,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, kb + (int64_t)(s + 1) * BK, g.ka_valid, tid);
           issue_b(s + 1);
         }
-        compute(smem + buf * Cfg::STAGE, [](int) {});
+        compute(smem + buf * Cfg::STAGE, smem + buf * Cfg::STAGE + Cfg::A_PART, [](int) {});
         if (more) sa.store(smem + (buf ^ 1) * Cfg::STAGE, tid);
         wait_vmcnt<0>();   // B's DMA of step s+1 has landed
         __syncthreads();   // A's LDS writes and B's DMA of step s+1 are complete
