@@ -31,18 +31,34 @@ struct Carver {
 __global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __restrict__ in, int64_t rows,
                                                             int64_t cols, int64_t ldi, uint16_t* __restrict__ out,
                                                             int64_t out_rows, int64_t out_cols, int64_t ldo) {
-  __shared__ uint16_t tile[64][65];
+  // 64 x 64 tile, moved in 16-byte pieces (8 bf16): thread t reads row
+  // i0 + t/8 (+32) at columns j0 + 8 (t%8), and writes output row j0 + t/8
+  // (+32) at columns i0 + 8 (t%8).  cols, ldi, out_cols and ldo are
+  // multiples of 8 (model dimensions), so a piece is wholly inside or outside.
+  // The LDS rows are padded to 72 elements so that the column reads of the
+  // write phase fall in distinct banks.
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64][72];
   const int64_t i0 = (int64_t)blockIdx.x * 64, j0 = (int64_t)blockIdx.y * 64;
-  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-    const int a = e / 64, b = e % 64;
-    const int64_t i = i0 + a, j = j0 + b;
-    tile[a][b] = (i < rows && j < cols) ? in[i * ldi + j] : (uint16_t)0;
+  const int r = threadIdx.x / 8, c = threadIdx.x % 8;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int a = r + 32 * h;
+    const int64_t i = i0 + a, j = j0 + 8 * c;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (i < rows && j < cols) v = *(const uint4*)(in + i * ldi + j);
+    *(uint4*)&tile[a][8 * c] = v;
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-    const int a = e / 64, b = e % 64;
-    const int64_t jj = j0 + a, ii = i0 + b;
-    if (jj < out_rows && ii < out_cols) out[jj * ldo + ii] = tile[b][a];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int a = r + 32 * h;                       // output row j0 + a = input column
+    const int64_t jj = j0 + a, ii = i0 + 8 * c;
+    if (jj < out_rows && ii < out_cols) {
+      uint32_t w[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) w[q] = (uint32_t)tile[8 * c + 2 * q][a] | ((uint32_t)tile[8 * c + 2 * q + 1][a] << 16);
+      *(uint4*)(out + jj * ldo + ii) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
   }
 }
 
