@@ -9,15 +9,17 @@
 namespace elas {
 
 template <bool RAW>
-__global__ __launch_bounds__(256) void sparsify24_kernel(const uint16_t* __restrict__ h, int64_t M,
-                                                         int64_t N, int64_t chunks, uint16_t* __restrict__ vals,
-                                                         uint8_t* __restrict__ meta, int64_t ldv,
-                                                         int64_t ldm) {
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= M * chunks) return;
-  const int64_t row = t / chunks;
-  const int64_t c = t - row * chunks;
-  const int64_t f0 = c * 16;
+__global__ __launch_bounds__(256) void sparsify24_kernel(const uint16_t* __restrict__ h, int64_t row0, uint32_t rows,
+                                                         int64_t N, uint32_t chunks, uint16_t* __restrict__ vals,
+                                                         uint8_t* __restrict__ meta, int64_t ldv, int64_t ldm) {
+  // rows * chunks < 2^31 (the host cuts larger inputs into slabs), so the
+  // thread -> (row, chunk) split uses 32-bit arithmetic.
+  const uint32_t t = blockIdx.x * 256u + threadIdx.x;
+  if (t >= rows * chunks) return;
+  const uint32_t rl = t / chunks;
+  const uint32_t c = t - rl * chunks;
+  const int64_t row = row0 + rl;
+  const int64_t f0 = (int64_t)c * 16;
   const uint16_t* src = h + row * N + f0;
   u32x4 lo = {0u, 0u, 0u, 0u}, hi = {0u, 0u, 0u, 0u};
   // N % 8 == 0, so each 8-feature half is entirely inside or entirely past
@@ -30,25 +32,26 @@ __global__ __launch_bounds__(256) void sparsify24_kernel(const uint16_t* __restr
   uint32_t code16 = 0u;
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
-    const uint32_t e0 = w[2 * g] & 0xFFFFu, e1 = w[2 * g] >> 16;
-    const uint32_t e2 = w[2 * g + 1] & 0xFFFFu, e3 = w[2 * g + 1] >> 16;
     uint32_t code, pair;
     if constexpr (RAW) {
-      code = top2_code(e0 & 0x7FFFu, e1 & 0x7FFFu, e2 & 0x7FFFu, e3 & 0x7FFFu);
-      pair = pick_pair(code, e0, e1, e2, e3);
+      // rank |h| (sign bit cleared); keep the signed values
+      const Top2 k = top2_keys(w[2 * g] & 0x7FFF7FFFu, w[2 * g + 1] & 0x7FFF7FFFu);
+      code = top2_code_of(k);
+      pair = pick_pair(code, w[2 * g] & 0xFFFFu, w[2 * g] >> 16, w[2 * g + 1] & 0xFFFFu, w[2 * g + 1] >> 16);
     } else {
-      const uint32_t r0 = relu_bits(e0), r1 = relu_bits(e1), r2 = relu_bits(e2), r3 = relu_bits(e3);
-      code = top2_code(r0, r1, r2, r3);
-      const uint32_t kept = pick_pair(code, r0, r1, r2, r3);
-      const float a = bf16_to_f32(kept & 0xFFFFu), b = bf16_to_f32(kept >> 16);
-      pair = f32_to_bf16_rne(a * a) | (f32_to_bf16_rne(b * b) << 16);
+      // relu (NaN -> 0), rank by value with ties to the lower index, keep
+      // relu(h)^2 rounded to bf16
+      const Top2 k = top2_keys(relu_bits2(w[2 * g]), relu_bits2(w[2 * g + 1]));
+      code = top2_code_of(k);
+      const float a = __builtin_bit_cast(float, k.first << 16), b = __builtin_bit_cast(float, k.second << 16);
+      pair = bf16x2_rne(a * a, b * b);
     }
     out[g] = pair;
     code16 |= code << (4 * g);
   }
   uint4 o = {out[0], out[1], out[2], out[3]};
-  *(uint4*)(vals + row * ldv + c * 8) = o;
-  *(uint16_t*)(meta + row * ldm + c * 2) = (uint16_t)code16;
+  *(uint4*)(vals + row * ldv + (int64_t)c * 8) = o;
+  *(uint16_t*)(meta + row * ldm + (int64_t)c * 2) = (uint16_t)code16;
 }
 
 hipError_t launch_sparsify24(const uint16_t* h, int64_t M, int64_t N, bool raw, uint16_t* vals,
@@ -56,14 +59,21 @@ hipError_t launch_sparsify24(const uint16_t* h, int64_t M, int64_t N, bool raw, 
   if (M == 0) return hipSuccess;
   const int64_t ldv = vals_ld(N), ldm = meta_ld(N);
   const int64_t chunks = ldv / 8;             // 16 features per thread, padding included
-  const int64_t threads = M * chunks;
-  const dim3 grid((unsigned)((threads + 255) / 256)), block(256);
+  const int64_t slab = ((int64_t(1) << 31) - 1) / chunks;   // rows per launch: rows * chunks < 2^31
   TimedLaunch tl("sparsify24", stream);
-  if (raw)
-    hipLaunchKernelGGL(sparsify24_kernel<true>, grid, block, 0, stream, h, M, N, chunks, vals, meta, ldv, ldm);
-  else
-    hipLaunchKernelGGL(sparsify24_kernel<false>, grid, block, 0, stream, h, M, N, chunks, vals, meta, ldv, ldm);
-  return hipGetLastError();
+  for (int64_t r0 = 0; r0 < M; r0 += slab) {
+    const int64_t rows = M - r0 < slab ? M - r0 : slab;
+    const dim3 grid((unsigned)((rows * chunks + 255) / 256)), block(256);
+    if (raw)
+      hipLaunchKernelGGL(sparsify24_kernel<true>, grid, block, 0, stream, h, r0, (uint32_t)rows, N, (uint32_t)chunks,
+                         vals, meta, ldv, ldm);
+    else
+      hipLaunchKernelGGL(sparsify24_kernel<false>, grid, block, 0, stream, h, r0, (uint32_t)rows, N,
+                         (uint32_t)chunks, vals, meta, ldv, ldm);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace elas
