@@ -183,22 +183,18 @@ __device__ __forceinline__ int swz_row(int row, int chunk) {
 }
 
 // Expand 2 groups (4 kept values in 8 bytes + 2 codes in one byte) to 8 dense
-// bf16 values packed as a uint4.
+// bf16 values packed as a uint4: kept value v0 (v1) of a group lands in slot
+// i0 (i1) of its 4 by a 64-bit shift of 16 i0 (16 i1) bits, the other slots 0.
 __device__ __forceinline__ uint4 expand2(uint2 kept, uint32_t codes) {
-  uint32_t d[4];
+  uint64_t d[2];
 #pragma unroll
   for (int g = 0; g < 2; ++g) {
     const uint32_t pair = g ? kept.y : kept.x;
     const uint32_t code = (codes >> (4 * g)) & 0xFu;
-    const uint32_t i0 = code & 3u, i1 = code >> 2;
-    const uint32_t v0 = pair & 0xFFFFu, v1 = pair >> 16;
-    uint32_t e[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) e[s] = (i0 == (uint32_t)s ? v0 : 0u) | (i1 == (uint32_t)s ? v1 : 0u);
-    d[2 * g] = e[0] | (e[1] << 16);
-    d[2 * g + 1] = e[2] | (e[3] << 16);
+    const uint32_t s0 = (code & 3u) << 4, s1 = (code >> 2) << 4;
+    d[g] = ((uint64_t)(pair & 0xFFFFu) << s0) | ((uint64_t)(pair >> 16) << s1);
   }
-  return make_uint4(d[0], d[1], d[2], d[3]);
+  return make_uint4((uint32_t)d[0], (uint32_t)(d[0] >> 32), (uint32_t)d[1], (uint32_t)(d[1] >> 32));
 }
 
 // ---- direct global -> LDS staging ------------------------------------------
