@@ -427,7 +427,7 @@ struct StagerKMSP {
   static constexpr int NU = 64 * CHUNKS / NT;
   static_assert((64 * CHUNKS) % NT == 0, "units per thread");
   uint4 v[NU];
-  uint32_t m[NU];
+  uint16_t m[NU];
   __device__ __forceinline__ void load(const uint16_t* __restrict__ pv, int64_t ldv, const uint8_t* __restrict__ pm,
                                        int64_t ldm, int64_t col0, int64_t cols_valid, int64_t k0, int64_t k_valid,
                                        int tid) {
@@ -441,6 +441,29 @@ struct StagerKMSP {
         v[u] = *(const uint4*)(pv + gk * ldv + f / 2);
         m[u] = *(const uint16_t*)(pm + gk * ldm + f / 8);
       }
+    }
+  }
+  // Unchecked path (tile and step inside the matrix): per-lane byte offsets
+  // from the step's first row and the tile's first column, constant over the
+  // steps, and a wave-uniform base per step.
+  __device__ __forceinline__ static void lane_offs(int64_t ldv, int64_t ldm, int tid, uint32_t (&ov)[NU],
+                                                   uint32_t (&om)[NU]) {
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      const int q = u * NT + tid, k = q / CHUNKS, c = q % CHUNKS;
+      ov[u] = (uint32_t)k * (uint32_t)(ldv * 2) + (uint32_t)c * 16u;
+      om[u] = (uint32_t)k * (uint32_t)ldm + (uint32_t)c * 2u;
+    }
+  }
+  __device__ __forceinline__ void load_fast(const char* vbase, const char* mbase, const uint32_t (&ov)[NU],
+                                            const uint32_t (&om)[NU]) {
+    const char* vb = (const char*)uniform_ptr(vbase);
+    const char* mb = (const char*)uniform_ptr(mbase);
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      const u32x4 x = *(const __attribute__((address_space(1))) u32x4*)(vb + ov[u]);
+      v[u] = make_uint4(x[0], x[1], x[2], x[3]);
+      m[u] = *(const __attribute__((address_space(1))) uint16_t*)(mb + om[u]);
     }
   }
   __device__ __forceinline__ void store(char* lds, int tid) const {
@@ -1096,6 +1119,8 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     uint32_t offB[TB::PER_WAVE];
 #pragma unroll
     for (int j = 0; j < TB::PER_WAVE; ++j) offB[j] = TB::lane_off(j, g.ldb, wave, lane);
+    uint32_t aov[StagerKMSP<BM, NT>::NU], aom[StagerKMSP<BM, NT>::NU];
+    StagerKMSP<BM, NT>::lane_offs(g.lda, g.ldam, tid, aov, aom);
     // Accumulate steps [0, ns) of the K range starting at kb of the tile at (m0, n0).
     auto run_tile = [&](int64_t m0, int64_t n0, int64_t kb, int ns) __attribute__((always_inline)) {
       zero_acc();
@@ -1106,6 +1131,23 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         b_steps_in = k_in <= 0 ? 0 : (int)(k_in / BK < ns ? k_in / BK : ns);
       }
       b_steps_in = __builtin_amdgcn_readfirstlane(b_steps_in);
+      int a_steps_in = 0;   // steps whose A loads need no bounds checks
+      if (m0 + BM <= g.m_valid) {
+        const int64_t k_in = g.ka_valid - kb;
+        a_steps_in = k_in <= 0 ? 0 : (int)(k_in / BK < ns ? k_in / BK : ns);
+      }
+      a_steps_in = __builtin_amdgcn_readfirstlane(a_steps_in);
+      auto load_a = [&](int step) __attribute__((always_inline)) {
+        const int64_t k0 = kb + (int64_t)step * BK;
+        if (step < a_steps_in) {
+          sa.load_fast((const char*)(g.A + k0 * g.lda) + m0, (const char*)(g.Am + k0 * g.ldam + m0 / 8), aov, aom);
+        } else {
+          int64_t kc = uniform_i64(k0);   // addresses formed afresh (see the direct path)
+          int tc = tid;
+          asm volatile("" : "+s"(kc), "+v"(tc));
+          sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, kc, g.ka_valid, tc);
+        }
+      };
       auto issue_b = [&](int step) __attribute__((always_inline)) {
         const int64_t k0 = kb + (int64_t)step * BK;
         const uint32_t base = smem_lds + (uint32_t)((step & 1) * Cfg::STAGE) + Cfg::A_BYTES;
@@ -1115,7 +1157,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           TB::template issue<0, TB::PER_WAVE>(g.B, g.ldb, n0, g.N, k0, g.kb_valid, base, wave, lane);
       };
       if (ns > 0) {
-        sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, kb, g.ka_valid, tid);
+        load_a(0);
         issue_b(0);
         sa.store(smem, tid);
         wait_vmcnt<0>();
@@ -1125,7 +1167,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         const int buf = s & 1;
         const bool more = s + 1 < ns;
         if (more) {
-          sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, kb + (int64_t)(s + 1) * BK, g.ka_valid, tid);
+          load_a(s + 1);
           issue_b(s + 1);
         }
         compute(smem + buf * Cfg::STAGE, smem + buf * Cfg::STAGE + Cfg::A_PART, [](int) {});
