@@ -11,8 +11,10 @@ library on the launch stream during the timed steps:
   spgemm    -- the 2:4 sparse x dense down projection (v_smfmac);
   kernels   -- every kernel's launches, average time and rate;
 and, timed separately, the standalone sparsify kernel on h [65536 x 2736]
-(the 350M-shape activation) against the HBM peak, plus the CPU oracle on a
-bounded sample of the same workload (cpu_baseline).
+(the 350M-shape activation) against the HBM peak, the 2:4-compressed vs dense
+activation run at T = 262144 (large_batch), the forward-only comparison with
+the full-rank ReLU^2 FFN at the shapes of the paper's Table 3 (table3), plus
+the CPU oracle on a bounded sample of the same workload (cpu_baseline).
 """
 from __future__ import annotations
 
@@ -171,6 +173,118 @@ def large_batch_compare(steps: int, warmup: int) -> dict:
     return out
 
 
+# Table 3 (Sec. 4.2.3): FFN speed-up of ELAS over the full-rank FFN, printed
+# there as full-rank time / ELAS time for the four model sizes; kept as context.
+TABLE3_SEQ = [512, 2048, 4096, 8192, 16384, 32768, 65536]
+TABLE3_PAPER = {
+    "llama60m": [0.50, 1.57, 1.75, 1.50, 1.55, 1.59, 1.55],
+    "llama130m": [0.75, 1.56, 1.80, 1.52, 1.51, 1.53, 1.52],
+    "llama350m": [1.29, 1.87, 1.86, 1.82, 1.85, 1.88, 1.88],
+    "llama1b": [2.05, 2.47, 2.48, 2.55, 2.63, 2.73, 2.75],
+}
+
+
+def table3_compare(iters: int = 20, warmup: int = 3) -> dict:
+    """Forward-only ELAS FFN (2:4 activations) vs the full-rank ReLU^2 FFN
+    (elas_fullrank_ffn_fwd, dense MFMA) at the four model shapes and the token
+    counts of Table 3, as device time per call (see device_us).  The ELAS
+    entry point re-lays out its four weight factors on every call (one
+    launch of K-contiguous copies); `elas_weight_relayout_us` is that part of
+    its time.  The full-rank entry point takes its weights already
+    K-contiguous (linear-layer orientation)."""
+    import numpy as np
+    import torch
+
+    import paper_2605_03667_amd as elas
+    from synthetic import CONFIGS, config_inputs, fullrank_inputs
+
+    dev = torch.device("cuda:0")
+    Tmax = max(TABLE3_SEQ)
+
+    def to_dev(b):
+        return torch.from_numpy(np.ascontiguousarray(b).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    # Device time per call: the calls are queued behind a spin kernel, so the
+    # events bracket back-to-back GPU work rather than the host's launch rate.
+    a0, b0 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0.record()
+    torch.cuda._sleep(1 << 22)
+    b0.record()
+    torch.cuda.synchronize()
+    cycles_per_ms = (1 << 22) / max(a0.elapsed_time(b0), 1e-3)
+    host_bound = []
+
+    def device_us(fn, queue_ms=30.0):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        best = float("inf")
+        for _ in range(3):
+            torch.cuda._sleep(int(cycles_per_ms * queue_ms))
+            h0 = time.perf_counter()
+            a.record()
+            for _ in range(iters):
+                fn()
+            b.record()
+            host_ms = (time.perf_counter() - h0) * 1e3
+            torch.cuda.synchronize()
+            if host_ms > 0.8 * queue_ms:
+                host_bound.append(host_ms)
+            best = min(best, a.elapsed_time(b) / iters)
+        return best * 1e3
+
+    models = {}
+    for k, name in enumerate(TABLE3_PAPER):
+        c = CONFIGS[name]
+        d, F, r = c["d"], c["d_ff"], c["r"]
+        lo = config_inputs(name, T=Tmax, seed_base=40 + k)
+        lo.pop("dY")
+        fr = fullrank_inputs(0, d, F, c["d_ff_true"], seed_base=40 + k)
+        t = {n: to_dev(v) for n, v in lo.items()}
+        W_up, W_down = to_dev(fr["W_up"]), to_dev(fr["W_down"])
+        del lo, fr
+        bf = torch.bfloat16
+        o_lo = {"y": torch.empty((Tmax, d), dtype=bf, device=dev), "P": torch.empty((Tmax, r), dtype=bf, device=dev),
+                "s_vals": torch.empty((Tmax, elas.elas_vals_ld(F)), dtype=bf, device=dev),
+                "s_meta": torch.empty((Tmax, elas.elas_meta_ld(F)), dtype=torch.uint8, device=dev),
+                "Z": torch.empty((Tmax, r), dtype=bf, device=dev)}
+        o_fr = {"y": torch.empty((Tmax, d), dtype=bf, device=dev), "S": torch.empty((Tmax, F), dtype=bf, device=dev)}
+        ws = torch.empty(max(1, elas.elas_lowrank_ffn_fwd_workspace_bytes(Tmax, d, F, r)), dtype=torch.uint8,
+                         device=dev)
+        row = {"elas_us": [], "fullrank_us": [], "speedup": []}
+        for T in TABLE3_SEQ:
+            x = t["x"][:T]
+            ol = {n: v[:T] for n, v in o_lo.items()}
+            of = {n: v[:T] for n, v in o_fr.items()}
+            e = device_us(lambda: elas.elas_lowrank_ffn_fwd(x, t["U_up"], t["V_up"], t["U_down"], t["V_down"],
+                                                            out=ol, workspace=ws))
+            f = device_us(lambda: elas.elas_fullrank_ffn_fwd(x, W_up, W_down, out=of))
+            row["elas_us"].append(round(e, 2))
+            row["fullrank_us"].append(round(f, 2))
+            row["speedup"].append(round(f / e, 3))
+        # the per-call weight re-layout of the ELAS entry point
+        elas.elas_timing_enable(True)
+        for _ in range(iters):
+            elas.elas_lowrank_ffn_fwd(t["x"][:512], t["U_up"], t["V_up"], t["U_down"], t["V_down"],
+                                      out={n: v[:512] for n, v in o_lo.items()}, workspace=ws)
+        torch.cuda.synchronize()
+        elas.elas_timing_enable(False)
+        n_tr, ms_tr = elas.elas_timing_collect().get("weight_transpose", (0, 0.0))
+        row["elas_weight_relayout_us"] = round(ms_tr / iters * 1e3, 2)
+        T = Tmax
+        row["fullrank_tflops_at_max_T"] = round(4.0 * T * d * F / (row["fullrank_us"][-1] * 1e-6) / 1e12, 1)
+        row["elas_alg_tflops_at_max_T"] = round(T * (4.0 * d * r + 3.0 * r * F) / (row["elas_us"][-1] * 1e-6) / 1e12, 1)
+        row["shape"] = {"d": d, "d_ff": F, "d_ff_true": c["d_ff_true"], "r": r}
+        row["paper_speedup"] = TABLE3_PAPER[name]
+        models[name] = row
+        del t, W_up, W_down, o_lo, o_fr, ws
+        torch.cuda.empty_cache()
+    return {"seq": TABLE3_SEQ, "speedup_is": "fullrank_us / elas_us (forward only)",
+            "timing": f"device time per call, best of 3 runs of {iters} calls queued behind a spin kernel",
+            "host_bound_runs": len(host_bound), "models": models}
+
+
 def cpu_baseline(cfg: dict, sample_tokens: int) -> dict:
     import numpy as np
     from threadpoolctl import threadpool_info
@@ -199,6 +313,8 @@ def main() -> int:
     ap.add_argument("--no-sparsify", action="store_true", help="skip the standalone sparsify measurement")
     ap.add_argument("--no-large-batch", action="store_true",
                     help="skip the T = 262144 compressed-vs-dense activation comparison")
+    ap.add_argument("--no-table3", action="store_true",
+                    help="skip the forward-only ELAS vs full-rank FFN comparison (Table 3 shapes)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (known traffic) for HBM counter calibration")
     args = ap.parse_args()
@@ -338,6 +454,11 @@ def main() -> int:
         print("[bench] large batch (T = 262144): compressed vs dense activations", file=sys.stderr, flush=True)
         torch.cuda.empty_cache()
         result["large_batch"] = large_batch_compare(steps=5, warmup=2)
+
+    if not args.no_table3 and args.workload == "llama1b":
+        print("[bench] forward-only ELAS vs full-rank FFN (Table 3 shapes)", file=sys.stderr, flush=True)
+        torch.cuda.empty_cache()
+        result["table3"] = table3_compare()
 
     if args.copy_calibration:
         # a plain copy of known size: reads 1 GiB and writes 1 GiB per launch

@@ -190,6 +190,25 @@ int elas_lowrank_ffn_bwd(const uint16_t* dy, const uint16_t* x, const uint16_t* 
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * elas_fullrank_ffn_fwd -- forward of the full-rank ReLU^2 FFN, the block the
+ * paper's FFN speed-up table compares ELAS against (Table 3, Sec. 4.2.3).
+ * The weights are the full matrices W of Eq. 1 (acting on column vectors, as
+ * a linear layer stores them); with tokens as rows:
+ *
+ *     H = x W_up^T,   S = max(0,H)^2,   Y = S W_down^T
+ *
+ * Inputs (bf16, device, read only): x [T,d], W_up [d_ff,d], W_down [d,d_ff].
+ * Outputs (bf16, device, written): y [T,d] and S [T,d_ff], the dense
+ *   activation (what a training step would keep for its backward).
+ * Rounding points: H (before ReLU^2), S and y are rounded to bf16
+ * (nearest-even); both products accumulate in fp32.  No workspace.
+ * Requires T >= 0, d, d_ff > 0, multiples of 8 and at most 65536.  T == 0 is a
+ * no-op (pointers are then not inspected and may be NULL).
+ */
+int elas_fullrank_ffn_fwd(const uint16_t* x, const uint16_t* W_up, const uint16_t* W_down,
+                          int64_t T, int64_t d, int64_t d_ff, uint16_t* y, uint16_t* S, void* stream);
+
+/*
  * Per-kernel timing (diagnostics for benchmarks; not thread-safe).
  *
  * elas_timing_enable(1) clears earlier records and starts recording: every

@@ -83,6 +83,20 @@ def backward(dY, x, U_up, V_up, U_down, V_down, fwd, *, bf16io: bool = True,
             "dV_down": dV_down, "dZ": dZ, "dS": dS, "dH": dH, "dP": dP}
 
 
+def fullrank_forward(x, W_up, W_down, *, bf16io: bool = True):
+    """Forward of the full-rank ReLU^2 FFN that Table 3 (Sec. 4.2.3) compares
+    ELAS against.  W_up [d_ff, d] and W_down [d, d_ff] are the full matrices
+    W of Eq. 1 (acting on column vectors); with tokens as rows:
+    H = x W_up^T, S = relu(H)^2, Y = S W_down^T.  With ``bf16io`` H (before
+    ReLU^2), S and Y are rounded to bf16, the same points as the low-rank
+    block's H, S and Y.  Returns dict(Y, H, S)."""
+    rb = _rounder(bf16io)
+    H = rb(x @ W_up.T)
+    S = rb(relu2(H))
+    Y = rb(S @ W_down.T)
+    return {"Y": Y, "H": H, "S": S}
+
+
 def from_bits(inputs: dict) -> dict:
     """bf16 bit arrays -> exact float64 arrays (same keys)."""
     return {k: bf16.to_f64(v) for k, v in inputs.items()}

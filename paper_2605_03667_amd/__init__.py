@@ -66,6 +66,7 @@ _SIGNATURES = {
     "elas_lowrank_ffn_bwd_workspace_bytes": ([_i64, _i64, _i64, _i64, _u32], _sz),
     "elas_lowrank_ffn_bwd": ([_p] * 6 + [_i64] * 4 + [_u32] + [_p] * 4 + [_p] * 5 + [_p, _sz, _p],
                              ctypes.c_int),
+    "elas_fullrank_ffn_fwd": ([_p] * 3 + [_i64] * 3 + [_p] * 3, ctypes.c_int),
     "elas_timing_enable": ([ctypes.c_int], ctypes.c_int),
     "elas_timing_collect": ([], ctypes.c_int),
     "elas_timing_entry": ([ctypes.c_int, ctypes.c_char_p, ctypes.c_int, ctypes.POINTER(_i64),
@@ -235,6 +236,23 @@ def elas_lowrank_ffn_bwd(dy, x, U_up, V_up, U_down, V_down, saved: dict, flags: 
         _ptr(workspace, torch.uint8, "workspace"), 0 if workspace is None else workspace.numel(),
         _stream(dev)))
     return grads
+
+
+def elas_fullrank_ffn_fwd(x, W_up, W_down, out: dict | None = None) -> dict:
+    """Forward of the full-rank ReLU^2 FFN y = relu(x W_up^T)^2 W_down^T with
+    W_up [d_ff, d] and W_down [d, d_ff].  Returns dict(y, S), S being the
+    dense [T, d_ff] activation."""
+    T, d = x.shape
+    F = W_up.shape[0]
+    dev = x.device
+    if out is None:
+        out = {"y": torch.empty((T, d), dtype=torch.bfloat16, device=dev),
+               "S": torch.empty((T, F), dtype=torch.bfloat16, device=dev)}
+    bf = torch.bfloat16
+    _check(lib().elas_fullrank_ffn_fwd(
+        _ptr(x, bf, "x"), _ptr(W_up, bf, "W_up"), _ptr(W_down, bf, "W_down"), T, d, F,
+        _ptr(out["y"], bf, "y"), _ptr(out["S"], bf, "S"), _stream(dev)))
+    return out
 
 
 def elas_timing_enable(enable: bool = True) -> None:

@@ -215,4 +215,18 @@ int elas_lowrank_ffn_bwd(const uint16_t* dy, const uint16_t* x, const uint16_t* 
   return device_status(elas::run_bwd(a, (hipStream_t)stream), "backward launch");
 }
 
+int elas_fullrank_ffn_fwd(const uint16_t* x, const uint16_t* W_up, const uint16_t* W_down, int64_t T, int64_t d,
+                          int64_t d_ff, uint16_t* y, uint16_t* S, void* stream) {
+  g_last_error.clear();
+  ELAS_CHECK(check_ffn_dims(T, d, d_ff, 8));
+  if (T == 0) return ELAS_OK;
+  ELAS_CHECK(check_ptr(x, "x"));
+  ELAS_CHECK(check_ptr(W_up, "W_up"));
+  ELAS_CHECK(check_ptr(W_down, "W_down"));
+  ELAS_CHECK(check_ptr(y, "y"));
+  ELAS_CHECK(check_ptr(S, "S"));
+  return device_status(elas::run_fullrank_fwd(x, W_up, W_down, T, d, d_ff, y, S, (hipStream_t)stream),
+                       "full-rank forward launch");
+}
+
 }  // extern "C"

@@ -28,9 +28,22 @@ struct Carver {
 // ---- small kernels -----------------------------------------------------------
 
 // out[j][i] = in[i][j] for i < rows, j < cols; 0 elsewhere in [out_rows x out_cols].
-__global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __restrict__ in, int64_t rows,
-                                                            int64_t cols, int64_t ldi, uint16_t* __restrict__ out,
-                                                            int64_t out_rows, int64_t out_cols, int64_t ldo) {
+struct TransposeJob {
+  const uint16_t* in;
+  uint16_t* out;
+  int64_t rows, cols, ldi, out_rows, out_cols, ldo;
+  int tiles_x;      // 64-wide tiles along out_cols
+  int tile_begin;   // first flat tile index of this job
+};
+// Up to four transposes in one launch (the weight factors of one call): the
+// flat tile index selects the job, so small factors share the launch.
+constexpr int kMaxTransposeJobs = 4;
+struct TransposeBatch {
+  TransposeJob job[kMaxTransposeJobs];
+  int n;
+};
+
+__global__ __launch_bounds__(256) void transpose_pad_kernel(TransposeBatch tb) {
   // 64 x 64 tile, moved in 16-byte pieces (8 bf16): thread t reads row
   // i0 + t/8 (+32) at columns j0 + 8 (t%8), and writes output row j0 + t/8
   // (+32) at columns i0 + 8 (t%8).  cols, ldi, out_cols and ldo are
@@ -38,14 +51,20 @@ __global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __re
   // The LDS rows are padded to 72 elements so that the column reads of the
   // write phase fall in distinct banks.
   __shared__ __attribute__((aligned(16))) uint16_t tile[64][72];
-  const int64_t i0 = (int64_t)blockIdx.x * 64, j0 = (int64_t)blockIdx.y * 64;
+  int q = 0;
+#pragma unroll
+  for (int k = 1; k < kMaxTransposeJobs; ++k)
+    if (k < tb.n && (int)blockIdx.x >= tb.job[k].tile_begin) q = k;
+  const TransposeJob& jb = tb.job[q];
+  const int t = (int)blockIdx.x - jb.tile_begin;
+  const int64_t i0 = (int64_t)(t % jb.tiles_x) * 64, j0 = (int64_t)(t / jb.tiles_x) * 64;
   const int r = threadIdx.x / 8, c = threadIdx.x % 8;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int a = r + 32 * h;
     const int64_t i = i0 + a, j = j0 + 8 * c;
     uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if (i < rows && j < cols) v = *(const uint4*)(in + i * ldi + j);
+    if (i < jb.rows && j < jb.cols) v = *(const uint4*)(jb.in + i * jb.ldi + j);
     *(uint4*)&tile[a][8 * c] = v;
   }
   __syncthreads();
@@ -53,22 +72,38 @@ __global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __re
   for (int h = 0; h < 2; ++h) {
     const int a = r + 32 * h;                       // output row j0 + a = input column
     const int64_t jj = j0 + a, ii = i0 + 8 * c;
-    if (jj < out_rows && ii < out_cols) {
+    if (jj < jb.out_rows && ii < jb.out_cols) {
       uint32_t w[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) w[q] = (uint32_t)tile[8 * c + 2 * q][a] | ((uint32_t)tile[8 * c + 2 * q + 1][a] << 16);
-      *(uint4*)(out + jj * ldo + ii) = make_uint4(w[0], w[1], w[2], w[3]);
+      for (int k = 0; k < 4; ++k) w[k] = (uint32_t)tile[8 * c + 2 * k][a] | ((uint32_t)tile[8 * c + 2 * k + 1][a] << 16);
+      *(uint4*)(jb.out + jj * jb.ldo + ii) = make_uint4(w[0], w[1], w[2], w[3]);
     }
   }
 }
 
+// Collects transposes and launches them together.
+struct Transposes {
+  TransposeBatch tb{};
+  int tiles = 0;
+  void add(const uint16_t* in, int64_t rows, int64_t cols, int64_t ldi, uint16_t* out, int64_t out_rows,
+           int64_t out_cols, int64_t ldo) {
+    TransposeJob& j = tb.job[tb.n++];
+    j = TransposeJob{in, out, rows, cols, ldi, out_rows, out_cols, ldo, (int)cdiv(out_cols, 64), tiles};
+    tiles += j.tiles_x * (int)cdiv(out_rows, 64);
+  }
+  hipError_t launch(hipStream_t st) {
+    if (tiles == 0) return hipSuccess;
+    TimedLaunch tl("weight_transpose", st);
+    hipLaunchKernelGGL(transpose_pad_kernel, dim3((unsigned)tiles), dim3(256), 0, st, tb);
+    return hipGetLastError();
+  }
+};
+
 hipError_t transpose_pad(const uint16_t* in, int64_t rows, int64_t cols, int64_t ldi, uint16_t* out,
                          int64_t out_rows, int64_t out_cols, int64_t ldo, hipStream_t st) {
-  const dim3 grid((unsigned)cdiv(out_cols, 64), (unsigned)cdiv(out_rows, 64));
-  TimedLaunch tl("weight_transpose", st);
-  hipLaunchKernelGGL(transpose_pad_kernel, grid, dim3(256), 0, st, in, rows, cols, ldi, out, out_rows, out_cols,
-                     ldo);
-  return hipGetLastError();
+  Transposes t;
+  t.add(in, rows, cols, ldi, out, out_rows, out_cols, ldo);
+  return t.launch(st);
 }
 
 // Writes a 64 x 64 (m, n) tile of sums held as acc[i] = row m0 + ty + 16 i,
@@ -409,10 +444,12 @@ hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
   const int64_t T = a.T, d = a.d, F = a.F, r = a.r, Fp = pad64(F);
   const FwdWs w = fwd_ws((char*)a.ws, d, F, r);
   // Weight factors laid out K-contiguous for the MFMA operands.
-  ELAS_TRY(transpose_pad(a.U_up, d, r, r, w.U_upT, r, d, d, st));          // [r x d]
-  ELAS_TRY(transpose_pad(a.V_up, r, F, F, w.V_upT, Fp, r, r, st));         // [Fp x r], zero rows >= F
-  ELAS_TRY(transpose_pad(a.U_down, F, r, r, w.U_downT, r, Fp, Fp, st));    // [r x Fp], zero cols >= F
-  ELAS_TRY(transpose_pad(a.V_down, r, d, d, w.V_downT, d, r, r, st));      // [d x r]
+  Transposes tr;
+  tr.add(a.U_up, d, r, r, w.U_upT, r, d, d);          // [r x d]
+  tr.add(a.V_up, r, F, F, w.V_upT, Fp, r, r);         // [Fp x r], zero rows >= F
+  tr.add(a.U_down, F, r, r, w.U_downT, r, Fp, Fp);    // [r x Fp], zero cols >= F
+  tr.add(a.V_down, r, d, d, w.V_downT, d, r, r);      // [d x r]
+  ELAS_TRY(tr.launch(st));
   // P = x U_up
   ELAS_TRY(gemm_nt_bf16("k1_up_gemm", a.x, d, w.U_upT, d, a.P, r, T, r, d, st));
   if (!a.dense) {
@@ -440,6 +477,24 @@ hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
   }
   // Y = Z V_down
   ELAS_TRY(gemm_nt_bf16("k4_down_gemm", a.Z, r, w.V_downT, r, a.y, d, T, d, r, st));
+  return hipSuccess;
+}
+
+// Full-rank ReLU^2 FFN forward (the comparison of Table 3, Sec. 4.2.3).  The
+// weights come in the orientation of Eq. 1 (W_up [F x d], W_down [d x F]),
+// which is already the K-contiguous operand layout, so nothing is re-laid out:
+// S = relu(x W_up^T)^2 through the fused dense-activation epilogue of the
+// dense-mode up projection, then Y = S W_down^T.
+hipError_t run_fullrank_fwd(const uint16_t* x, const uint16_t* W_up, const uint16_t* W_down, int64_t T,
+                            int64_t d, int64_t F, uint16_t* y, uint16_t* S, hipStream_t st) {
+  // S^T = relu(W_up x^T)^2, written token-major [T x F]
+  GemmArgs g{};
+  g.A = W_up; g.lda = d; g.B = x; g.ldb = d;
+  g.M = F; g.N = T; g.K = d; g.m_valid = F; g.ka_valid = d; g.kb_valid = d;
+  g.act = S; g.ld_act = F; g.f_valid = F; g.act_square = 1;
+  ELAS_TRY(launch<CfgNT<256, EPI_ACT_DENSE, true, 2>>("fr_up_relu2", g, 1, st));
+  // Y = S W_down^T
+  ELAS_TRY(gemm_nt_bf16("fr_down_gemm", S, F, W_down, F, y, d, T, d, F, st));
   return hipSuccess;
 }
 

@@ -61,5 +61,7 @@ hipError_t run_spmm24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, 
                       hipStream_t stream);
 hipError_t run_fwd(const FfnArgs& a, hipStream_t stream);
 hipError_t run_bwd(const FfnArgs& a, hipStream_t stream);
+hipError_t run_fullrank_fwd(const uint16_t* x, const uint16_t* W_up, const uint16_t* W_down, int64_t T,
+                            int64_t d, int64_t F, uint16_t* y, uint16_t* S, hipStream_t stream);
 
 }  // namespace elas

@@ -77,6 +77,29 @@ def ffn_inputs(T: int, d: int, d_ff: int, r: int, d_ff_true: int | None = None,
     return out
 
 
+def fullrank_inputs(T: int, d: int, d_ff: int, d_ff_true: int | None = None, seed_base: int = 0) -> dict:
+    """Inputs of the full-rank ReLU^2 FFN forward, as bf16 bits.
+
+    Keys: x [T,d] ~ N(0,1); W_up [d_ff,d] ~ N(0,1/d), so that the
+    pre-activation is about N(0,1) as in the low-rank block; W_down [d,d_ff]
+    ~ N(0,1/d_ff_true).  Weights are in the orientation of a linear layer
+    (output features as rows).  Pad rows of W_up and pad columns of W_down
+    (feature index >= d_ff_true) are zero.
+    """
+    if d_ff_true is None:
+        d_ff_true = d_ff
+    s = 1000 * seed_base + 500
+    out = {
+        "x": normal_bf16((T, d), 1.0, s + 1),
+        "W_up": normal_bf16((d_ff, d), 1.0 / np.sqrt(d), s + 2),
+        "W_down": normal_bf16((d, d_ff), 1.0 / np.sqrt(d_ff_true), s + 3),
+    }
+    if d_ff_true < d_ff:
+        out["W_up"][d_ff_true:, :] = 0
+        out["W_down"][:, d_ff_true:] = 0
+    return out
+
+
 def config_inputs(name: str, T: int | None = None, seed_base: int | None = None) -> dict:
     """Inputs of a named workload; ``T`` overrides the token count."""
     c = dict(CONFIGS[name])

@@ -31,7 +31,7 @@ def _defines():
 
 def test_exports_every_declared_symbol():
     names = _declared()
-    assert len(names) == 14, names
+    assert len(names) == 15, names
     lib = ctypes.CDLL(elas.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -134,3 +134,18 @@ def test_bwd_validation():
     assert call(dy=None) == 1
     assert call(dV_down=MIS) == 3
     assert call(wsb=need - 1) == 4
+
+
+def test_fullrank_validation():
+    L = elas.lib()
+
+    def call(**kw):
+        a = dict(x=FAKE, T=16, d=32, F=64, y=FAKE)
+        a.update(kw)
+        return L.elas_fullrank_ffn_fwd(a["x"], FAKE, FAKE, a["T"], a["d"], a["F"], a["y"], FAKE, None)
+    assert call(d=12) == 2
+    assert call(F=60) == 2
+    assert call(T=-1) == 2
+    assert call(x=None) == 1
+    assert call(y=MIS) == 3
+    assert call(T=0, x=None, y=None) == 0     # no tokens: nothing inspected
