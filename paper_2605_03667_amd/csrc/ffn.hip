@@ -269,12 +269,40 @@ hipError_t launch(const char* tag, GemmArgs g, int splits, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Small problems: when 256-wide tiles would leave more than a quarter of the
+// CUs without a tile, 128 x 128 tiles (4 waves of 64 x 64) give four times as
+// many (twice as many for the staged 2:4 epilogues, which need 256 features).
+template <int EPI, bool M_FAST>
+using CfgNTs = GemmCfg<128, 128, 2, 2, OP_K, OP_K, EPI, M_FAST>;
+using CfgSPs = GemmCfg<128, 128, 2, 2, OP_SP, OP_K, EPI_BF16, false, 3, true, false, 64>;
+
+bool few_tiles(int64_t M, int64_t N, int bm, int bn) { return cdiv(M, bm) * cdiv(N, bn) * 4 < 3LL * device_cus(); }
+
+// 2:4 A times K-contiguous B, bf16 out.
+hipError_t launch_sp(const char* tag, const GemmArgs& g, hipStream_t st) {
+  if (few_tiles(g.M, g.N, 256, 256)) return launch<CfgSPs>(tag, g, 1, st);
+  return launch<CfgSP>(tag, g, 1, st);
+}
+// Epilogues that select and compress 2:4 groups (features along M).
+template <int EPI>
+hipError_t launch_staged(const char* tag, const GemmArgs& g, hipStream_t st) {
+  if (few_tiles(g.M, g.N, 256, 256)) return launch<CfgNT<128, EPI, true>>(tag, g, 1, st);
+  return launch<CfgNT<256, EPI, true>>(tag, g, 1, st);
+}
+// Epilogues that write or read the dense activation (features along M).
+template <int EPI>
+hipError_t launch_act(const char* tag, const GemmArgs& g, hipStream_t st) {
+  if (few_tiles(g.M, g.N, 256, 256)) return launch<CfgNTs<EPI, true>>(tag, g, 1, st);
+  return launch<CfgNT<256, EPI, true, 2>>(tag, g, 1, st);
+}
+
 // Dense product C[M x N] = A[M x K] * Bt[N x K]^T in bf16.
 hipError_t gemm_nt_bf16(const char* tag, const uint16_t* A, int64_t lda, const uint16_t* Bt, int64_t ldb, uint16_t* C, int64_t ldc,
                         int64_t M, int64_t N, int64_t K, hipStream_t st) {
   GemmArgs g{};
   g.A = A; g.lda = lda; g.B = Bt; g.ldb = ldb; g.C = C; g.ldc = ldc;
   g.M = M; g.N = N; g.K = K; g.m_valid = M; g.ka_valid = K; g.kb_valid = K;
+  if (few_tiles(M, N, 256, N <= 128 ? 128 : 256)) return launch<CfgNTs<EPI_BF16, false>>(tag, g, 1, st);
   if (N <= 128) return launch<CfgNT<128, EPI_BF16, false>>(tag, g, 1, st);
   return launch<CfgNT3>(tag, g, 1, st);
 }
@@ -437,7 +465,7 @@ hipError_t run_spmm24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, 
   g.B = bt; g.ldb = ldb;
   g.M = M; g.N = N; g.K = pad64(K); g.m_valid = M; g.ka_valid = pad64(K); g.kb_valid = K;
   g.C = c; g.ldc = N;
-  return launch<CfgSP>("spmm24", g, 1, st);
+  return launch_sp("spmm24", g, st);
 }
 
 hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
@@ -458,21 +486,21 @@ hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
     g.A = w.V_upT; g.lda = r; g.B = a.P; g.ldb = r;
     g.M = Fp; g.N = T; g.K = r; g.m_valid = Fp; g.ka_valid = r; g.kb_valid = r;
     g.sv = a.s_vals; g.sm = a.s_meta; g.ldv = vals_ld(F); g.ldm = meta_ld(F);
-    ELAS_TRY(launch<CfgNT<256, EPI_SPARSIFY, true>>("k2_up_relu2_sparsify", g, 1, st));
+    ELAS_TRY(launch_staged<EPI_SPARSIFY>("k2_up_relu2_sparsify", g, st));
     // Z = S U_down on the 2:4 operand
     GemmArgs z{};
     z.A = a.s_vals; z.lda = vals_ld(F); z.Am = a.s_meta; z.ldam = meta_ld(F);
     z.B = w.U_downT; z.ldb = Fp;
     z.M = T; z.N = r; z.K = Fp; z.m_valid = T; z.ka_valid = Fp; z.kb_valid = Fp;
     z.C = a.Z; z.ldc = r;
-    ELAS_TRY(launch<CfgSP>("k3_spmm_down", z, 1, st));
+    ELAS_TRY(launch_sp("k3_spmm_down", z, st));
   } else {
     // dense activations: S = relu(H)^2 written [T x F], then a dense product
     GemmArgs g{};
     g.A = w.V_upT; g.lda = r; g.B = a.P; g.ldb = r;
     g.M = Fp; g.N = T; g.K = r; g.m_valid = Fp; g.ka_valid = r; g.kb_valid = r;
     g.act = a.s_vals; g.ld_act = F; g.f_valid = F; g.act_square = 1;
-    ELAS_TRY(launch<CfgNT<256, EPI_ACT_DENSE, true, 2>>("k2_up_relu2_dense", g, 1, st));
+    ELAS_TRY(launch_act<EPI_ACT_DENSE>("k2_up_relu2_dense", g, st));
     ELAS_TRY(gemm_nt_bf16("k3_down_gemm_dense", a.s_vals, F, w.U_downT, Fp, a.Z, r, T, r, F, st));
   }
   // Y = Z V_down
@@ -492,7 +520,7 @@ hipError_t run_fullrank_fwd(const uint16_t* x, const uint16_t* W_up, const uint1
   g.A = W_up; g.lda = d; g.B = x; g.ldb = d;
   g.M = F; g.N = T; g.K = d; g.m_valid = F; g.ka_valid = d; g.kb_valid = d;
   g.act = S; g.ld_act = F; g.f_valid = F; g.act_square = 1;
-  ELAS_TRY(launch<CfgNT<256, EPI_ACT_DENSE, true, 2>>("fr_up_relu2", g, 1, st));
+  ELAS_TRY(launch_act<EPI_ACT_DENSE>("fr_up_relu2", g, st));
   // Y = S W_down^T
   ELAS_TRY(gemm_nt_bf16("fr_down_gemm", S, F, W_down, F, y, d, T, d, F, st));
   return hipSuccess;
@@ -519,7 +547,7 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
     g.A = a.U_down; g.lda = r; g.B = w.dZ; g.ldb = r;
     g.M = Fp; g.N = T; g.K = r; g.m_valid = F; g.ka_valid = r; g.kb_valid = r;
     g.sv = a.s_vals; g.sm = a.s_meta; g.ldv = ldv; g.ldm = ldm; g.dv = w.dH;
-    ELAS_TRY(launch<CfgNT<256, EPI_DH, true>>("b3_dH_masked", g, 1, st));
+    ELAS_TRY(launch_staged<EPI_DH>("b3_dH_masked", g, st));
     // dU_down = S^T dZ from the compressed S
     ELAS_TRY(gemm_tt_f32<OP_TSP>("b4_dU_down", a.s_vals, ldv, a.s_meta, ldm, w.dZ, r, Fp, r, T, w.part, a.dU_down, F,
                                  false, r, st));
@@ -529,7 +557,7 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
     p.B = a.V_up; p.ldb = F;
     p.M = T; p.N = r; p.K = Fp; p.m_valid = T; p.ka_valid = Fp; p.kb_valid = F;
     p.C = w.dP; p.ldc = r;
-    ELAS_TRY(launch<CfgSP>("b5_spmm_dP", p, 1, st));
+    ELAS_TRY(launch_sp("b5_spmm_dP", p, st));
     // dV_up = P^T dH, computed as dV_up^T = dH^T P and written transposed
     ELAS_TRY(gemm_tt_f32<OP_TSP>("b6_dV_up", w.dH, ldv, a.s_meta, ldm, a.P_in, r, Fp, r, T, w.part, a.dV_up, F, true, F,
                                  st));
@@ -545,7 +573,7 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
       h.A = w.V_upT; h.lda = r; h.B = a.P_in; h.ldb = r;
       h.M = Fp; h.N = T; h.K = r; h.m_valid = Fp; h.ka_valid = r; h.kb_valid = r;
       h.act = w.R; h.ld_act = F; h.f_valid = F; h.act_square = 0;
-      ELAS_TRY(launch<CfgNT<256, EPI_ACT_DENSE, true, 2>>("b3_relu_h_recompute", h, 1, st));
+      ELAS_TRY(launch_act<EPI_ACT_DENSE>("b3_relu_h_recompute", h, st));
       act = w.R;
       square = 0;
     }
@@ -553,7 +581,7 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
     g.A = a.U_down; g.lda = r; g.B = w.dZ; g.ldb = r;
     g.M = Fp; g.N = T; g.K = r; g.m_valid = F; g.ka_valid = r; g.kb_valid = r;
     g.act = const_cast<uint16_t*>(act); g.ld_act = F; g.f_valid = F; g.act_square = square; g.dact = w.dH;
-    ELAS_TRY(launch<CfgNT<256, EPI_DH_DENSE, true, 2>>(a.ste ? "b3_dH_ste" : "b3_dH_dense", g, 1, st));
+    ELAS_TRY(launch_act<EPI_DH_DENSE>(a.ste ? "b3_dH_ste" : "b3_dH_dense", g, st));
     if (a.dense) {
       // dU_down = S^T dZ with the dense S
       ELAS_TRY(gemm_tt_f32<OP_T>("b4_dU_down_dense", a.s_vals, F, nullptr, 0, w.dZ, r, F, r, T, w.part, a.dU_down, F,
