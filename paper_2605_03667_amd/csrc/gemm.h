@@ -149,10 +149,16 @@ struct GemmCfg {
   // stages.
   static constexpr bool STAGED_EPI = EPI_ == EPI_SPARSIFY || EPI_ == EPI_DH;
   static constexpr int META_PITCH = BM_ / 8 + 4;
+  // EPI_DH copies the stored S tile by DMA during the tile's last K step (the
+  // uniform two-stage ring only): the metadata rows go in as dword DMAs of 256
+  // bytes, META_DMA_PER_WAVE per wave, so their area is rounded up to that.
+  static constexpr bool PRE_S = EPI_ == EPI_DH && DEEP_ == 0 && STAGES_ == 2;
+  static constexpr int META_DMA_PER_WAVE = (BN_ * META_PITCH / 4 + 64 * NW - 1) / (64 * NW);
+  static constexpr int META_BYTES = PRE_S ? META_DMA_PER_WAVE * NW * 256 : (BN_ * META_PITCH + 15) / 16 * 16;
   static constexpr int A_PART = A_BYTES + AM_BYTES;   // one stage of A (and its metadata)
   static constexpr int LDS_BYTES = DEEP_ == 1   ? 3 * A_PART + 2 * B_BYTES
                                    : DEEP_ == 2 ? 2 * A_PART + 3 * B_BYTES
-                                                : STAGES_ * STAGE + (STAGED_EPI ? (BN_ * META_PITCH + 15) / 16 * 16 : 0);
+                                                : STAGES_ * STAGE + (STAGED_EPI ? META_BYTES : 0);
   static_assert(DEEP_ == 0 || (STAGES_ == 2 && !STAGED_EPI && DIRECT), "three-stage ring: plain epilogues, direct staging");
   static_assert(!STAGED_EPI || (BM_ == 256 && BN_ * BM_ <= STAGE && DIRECT), "staged epilogue layout");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
@@ -642,7 +648,10 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
   // is filling (the staged epilogues use it).  EPI_F32 writes a stream-K
   // partial tile to f32_slot when it is set, else the split's partial rows.
   float* f32_slot = nullptr;
-  auto epilogue = [&](const int64_t m0, const int64_t n0, char* stage) __attribute__((always_inline)) {
+  // `pre` runs in the staged epilogues once every wave has finished the
+  // main loop's LDS reads (EPI_DH with PRE_S: it issues the next tile's first
+  // loads and waits for the S tile copied during the last K step).
+  auto epilogue = [&](const int64_t m0, const int64_t n0, char* stage, auto&& pre) __attribute__((always_inline)) {
     if constexpr (Cfg::SWAP) {
       // Accumulator 4b+q of lane l is C[row l%32][col 8b + 4h + q] of its 32x32
       // block (h = l / 32).  N is a multiple of 8, so each 8-column (bf16) or
@@ -811,7 +820,10 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       const int64_t f_end = g.M - m0;                      // valid features (multiple of 64)
       __syncthreads();                                     // main-loop LDS reads are finished
 
-      if constexpr (Cfg::EPI == EPI_DH) {
+      if constexpr (Cfg::PRE_S) {
+        pre();            // the S tile is in LDS (copied during the last K step)
+        __syncthreads();
+      } else if constexpr (Cfg::EPI == EPI_DH) {
         // stored S rows of this tile -> LDS
         constexpr int VCH = BN * (BM / 16);               // 16-byte value chunks
 #pragma unroll
@@ -1051,7 +1063,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           ahead_deep(s + 2, gs + s + 2);
           compute(smem + a_off(gs + s), smem + b_off(gs + s), [](int) {});
         }
-        epilogue(m0, n0, smem);
+        epilogue(m0, n0, smem, [] {});
         if (!has_next) break;
         gs += nsteps;
         tile = next;
@@ -1066,6 +1078,66 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       // Stage (gs + s) % STAGES holds step s, A part then B part; step s
       // issues the loads STAGES - 1 steps ahead.
       auto st_off = [](int q) { return (uint32_t)((q % STAGES) * Cfg::STAGE); };
+      // PRE_S: the stored S rows of the tile at (m0, n0) -> LDS by DMA, values
+      // to the stage buffer at byte offset `off` (token row t's 16-byte chunk c
+      // at chunk position c ^ (t % 16), the layout the epilogue reads) and
+      // metadata rows to the area after the stages (pitch META_PITCH bytes).
+      // Lanes whose piece lies outside the matrix (or in a row's pad dword)
+      // copy the zero block.
+      auto issue_s_tile = [&](int64_t tm0, int64_t tn0, uint32_t off) __attribute__((always_inline)) {
+        if constexpr (Cfg::PRE_S) {
+          const int64_t t_end = g.N - tn0, f_end = g.M - tm0;
+          constexpr int VPW = BN * BM / 1024 / NW;    // 1 KB value blocks per wave
+          static_assert((BN * BM / 1024) % NW == 0, "value blocks per wave");
+          constexpr int MPD = Cfg::META_PITCH / 4;    // dwords per metadata row (the last is pad)
+          constexpr int MPW = Cfg::META_DMA_PER_WAVE;
+          const uint32_t lm_off = STAGES * Cfg::STAGE;
+          if (__builtin_amdgcn_readfirstlane((int)(t_end >= BN && f_end >= BM))) {
+            // whole tile inside: wave-uniform bases, 32-bit lane offsets; pad
+            // and surplus metadata lanes re-read their row's first dword
+            const char* vbase = (const char*)(g.sv + tn0 * g.ldv + tm0 / 2);
+            const char* mbase = (const char*)(g.sm + tn0 * g.ldm + tm0 / 8);
+#pragma unroll
+            for (int j = 0; j < VPW; ++j) {
+              const int blk = wave * VPW + j;
+              const int b = blk * 1024 + lane * 16;
+              const int row = b / BM, c = ((b % BM) / 16) ^ (row & 15);
+              dma_b128_s(vbase, (uint32_t)row * (uint32_t)(g.ldv * 2) + (uint32_t)c * 16u, smem_lds + off + blk * 1024);
+            }
+#pragma unroll
+            for (int j = 0; j < MPW; ++j) {
+              const int blk = wave * MPW + j;
+              const int q = blk * 64 + lane, row = q / MPD, w = q % MPD;
+              const bool real = row < BN && w < MPD - 1;
+              dma_b32_s(mbase, real ? (uint32_t)row * (uint32_t)g.ldm + 4u * (uint32_t)w : 0u,
+                        smem_lds + lm_off + blk * 256);
+            }
+          } else {
+            // edge tile: checked addresses (lane index laundered so that they
+            // are formed here rather than kept live across the main loop)
+            int lc = lane;
+            asm volatile("" : "+v"(lc));
+#pragma unroll
+            for (int j = 0; j < VPW; ++j) {
+              const int blk = wave * VPW + j;
+              const int b = blk * 1024 + lc * 16;
+              const int row = b / BM, c = ((b % BM) / 16) ^ (row & 15);
+              const void* src = (row < t_end && c * 16 < f_end) ? (const void*)(g.sv + (tn0 + row) * g.ldv + tm0 / 2 + c * 8)
+                                                                : (const void*)g_dma_zero;
+              dma_b128(src, __builtin_amdgcn_readfirstlane(smem_lds + off + blk * 1024));
+            }
+#pragma unroll
+            for (int j = 0; j < MPW; ++j) {
+              const int blk = wave * MPW + j;
+              const int q = blk * 64 + lc, row = q / MPD, w = q % MPD;
+              const void* src = (row < BN && row < t_end && w < MPD - 1 && 32 * w < f_end)
+                                    ? (const void*)(g.sm + (tn0 + row) * g.ldm + tm0 / 8 + 4 * w)
+                                    : (const void*)g_dma_zero;
+              dma_b32(src, __builtin_amdgcn_readfirstlane(smem_lds + lm_off + blk * 256));
+            }
+          }
+        }
+      };
 #pragma unroll
       for (int p = 0; p < STAGES - 1; ++p) {
         ahead_a(p, st_off(p));
@@ -1092,15 +1164,36 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             wait_vmcnt<0>();
           lds_barrier();   // every wave's loads of step s landed; step s-1's reads are done
           const int la = s + STAGES - 1;
-          ahead_a(la, st_off(gs + la));
-          ahead_b(la, st_off(gs + la) + Cfg::A_PART);
+          if (Cfg::PRE_S && la == nsteps) {
+            // last step: the free buffer takes this tile's S rows instead of
+            // the next tile's first step
+            issue_s_tile(m0, n0, st_off(gs + la));
+          } else {
+            ahead_a(la, st_off(gs + la));
+            ahead_b(la, st_off(gs + la) + Cfg::A_PART);
+          }
           const char* st = smem + st_off(gs + s);
           compute(st, st + Cfg::A_PART, [](int) {});
         }
-        const int last = nsteps > 0 ? (gs + nsteps - 1) % STAGES : 0;
-        epilogue(m0, n0, smem + last * Cfg::STAGE);
+        if constexpr (Cfg::PRE_S) {
+          // the next tile's first step goes to the buffer the last step read
+          // (every wave is past those reads when `pre` runs); this tile's S
+          // rows, issued before it, have landed once at most its LOADS remain
+          const uint32_t q0 = st_off(gs + nsteps - 1);
+          epilogue(m0, n0, smem + st_off(gs + nsteps), [&] {
+            ahead_a(nsteps, q0);
+            ahead_b(nsteps, q0 + Cfg::A_PART);
+            if (has_next)
+              wait_vmcnt<LOADS>();
+            else
+              wait_vmcnt<0>();
+          });
+        } else {
+          const int last = nsteps > 0 ? (gs + nsteps - 1) % STAGES : 0;
+          epilogue(m0, n0, smem + last * Cfg::STAGE, [] {});
+        }
         if (!has_next) break;
-        gs += nsteps;
+        gs += Cfg::PRE_S ? nsteps - 1 : nsteps;
         tile = next;
         m0 = nm0;
         n0 = nn0;
@@ -1190,13 +1283,13 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         origin(t, m0, n0);
         run_tile(m0, n0, k_first * BK, (int)(k_last - k_first));
         f32_slot = (float*)g.C + ((int64_t)blockIdx.x * g.stream_segs + (t - t_first)) * (BM * BN);
-        epilogue(m0, n0, smem);
+        epilogue(m0, n0, smem, [] {});
         it = (int64_t)t * S + k_last;
       }
     } else {
       origin(xcd_remap(blockIdx.x, ntiles), m0, n0);
       run_tile(m0, n0, kbeg, nsteps);
-      epilogue(m0, n0, smem);
+      epilogue(m0, n0, smem, [] {});
     }
   }
 }
