@@ -2,6 +2,8 @@
 // Fig. 1 caption; Eq. 1-3, Algorithm 1), backward (Sec. 3.3.2, Sec. 3.4) and
 // the standalone 2:4 sparse x dense product.  Everything runs on the caller's
 // stream in the caller's workspace; nothing here allocates.
+#include <algorithm>
+
 #include "gemm.h"
 #include "internal.h"
 
@@ -165,6 +167,23 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   reduce_store(acc, m0, n0, tx, ty, N, rows_out, transpose, out, ldo, tile);
 }
 
+// bf16 result of a split-K product with a bf16 output: out[m][n] =
+// bf16(sum over the splits k, in order, of part[k][m][n]); one 4-column piece
+// per thread (N and ldo are multiples of 8).
+__global__ __launch_bounds__(256) void splitk_reduce_bf16_kernel(const float* __restrict__ part, int splits, int64_t M,
+                                                                int64_t N, uint16_t* __restrict__ out, int64_t ldo) {
+  const int64_t pieces = N / 4;
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= M * pieces) return;
+  const int64_t m = q / pieces, n = (q % pieces) * 4;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int k = 0; k < splits; ++k) {
+    const float4 v = *(const float4*)(part + ((int64_t)k * M + m) * N + n);
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  *(uint2*)(out + m * ldo + n) = make_uint2(bf16x2_rne(acc.x, acc.y), bf16x2_rne(acc.z, acc.w));
+}
+
 // The stream-K counterpart: workgroup w of `wgs` owns iterations
 // [w I / wgs, (w+1) I / wgs) of the I = ntiles x S (tile, K step) space and
 // wrote the partial of the j-th tile it touched to part + (w segs + j) 256^2
@@ -272,15 +291,59 @@ hipError_t launch(const char* tag, GemmArgs g, int splits, hipStream_t st) {
 // Small problems: when 256-wide tiles would leave more than a quarter of the
 // CUs without a tile, 128 x 128 tiles (4 waves of 64 x 64) give four times as
 // many (twice as many for the staged 2:4 epilogues, which need 256 features).
-template <int EPI, bool M_FAST>
-using CfgNTs = GemmCfg<128, 128, 2, 2, OP_K, OP_K, EPI, M_FAST>;
 using CfgSPs = GemmCfg<128, 128, 2, 2, OP_SP, OP_K, EPI_BF16, false, 3, true, false, 64>;
 
 bool few_tiles(int64_t M, int64_t N, int bm, int bn) { return cdiv(M, bm) * cdiv(N, bn) * 4 < 3LL * device_cus(); }
 
-// 2:4 A times K-contiguous B, bf16 out.
-hipError_t launch_sp(const char* tag, const GemmArgs& g, hipStream_t st) {
-  if (few_tiles(g.M, g.N, 256, 256)) return launch<CfgSPs>(tag, g, 1, st);
+// Split-K of a bf16-output product with few 128 x 128 tiles and a long K:
+// enough splits to cover the CUs once, each at least 8 K steps of bk; the fp32
+// partials [splits x M x N] are then summed in split order and rounded once.
+struct SmallSplit {
+  int splits;
+  int64_t k_split;
+};
+SmallSplit plan_small_split(int64_t M, int64_t N, int64_t K, int bk) {
+  const int64_t tiles = cdiv(M, 128) * cdiv(N, 128), cus = device_cus();
+  const int64_t steps = cdiv(K, bk);
+  if (tiles * 2 > cus || steps < 16) return {1, K};
+  int64_t s = cus / tiles;
+  if (s > steps / 8) s = steps / 8;
+  if (s < 2) return {1, K};
+  const int64_t k_split = cdiv(cdiv(K, s), bk) * bk;
+  return {(int)cdiv(K, k_split), k_split};
+}
+size_t small_split_bytes(int64_t M, int64_t N, int64_t K, int bk) {
+  const SmallSplit p = plan_small_split(M, N, K, bk);
+  return p.splits > 1 ? (size_t)p.splits * M * N * sizeof(float) : 0;
+}
+template <int EPI, bool M_FAST>
+using CfgNTs = GemmCfg<128, 128, 2, 2, OP_K, OP_K, EPI, M_FAST>;
+using CfgSPsf = GemmCfg<128, 128, 2, 2, OP_SP, OP_K, EPI_F32, false, 3, true, false, 64>;
+
+hipError_t reduce_bf16(const float* part, int splits, int64_t M, int64_t N, uint16_t* out, int64_t ldo,
+                       hipStream_t st) {
+  TimedLaunch tl("splitk_reduce_bf16", st);
+  hipLaunchKernelGGL(splitk_reduce_bf16_kernel, dim3((unsigned)cdiv(M * (N / 4), 256)), dim3(256), 0, st, part, splits,
+                     M, N, out, ldo);
+  return hipGetLastError();
+}
+
+// 2:4 A times K-contiguous B, bf16 out (`part`: split-K partials, may be null).
+hipError_t launch_sp(const char* tag, GemmArgs g, hipStream_t st, float* part = nullptr) {
+  if (few_tiles(g.M, g.N, 256, 256)) {
+    const SmallSplit p = part ? plan_small_split(g.M, g.N, g.K, CfgSPsf::BK) : SmallSplit{1, g.K};
+    if (p.splits > 1) {
+      uint16_t* out = (uint16_t*)g.C;
+      const int64_t ldo = g.ldc;
+      g.C = part;
+      g.ldc = g.N;
+      g.k_split = p.k_split;
+      hipError_t e = launch<CfgSPsf>(tag, g, p.splits, st);
+      if (e != hipSuccess) return e;
+      return reduce_bf16(part, p.splits, g.M, g.N, out, ldo, st);
+    }
+    return launch<CfgSPs>(tag, g, 1, st);
+  }
   return launch<CfgSP>(tag, g, 1, st);
 }
 // Epilogues that select and compress 2:4 groups (features along M).
@@ -296,13 +359,25 @@ hipError_t launch_act(const char* tag, const GemmArgs& g, hipStream_t st) {
   return launch<CfgNT<256, EPI, true, 2>>(tag, g, 1, st);
 }
 
-// Dense product C[M x N] = A[M x K] * Bt[N x K]^T in bf16.
+// Dense product C[M x N] = A[M x K] * Bt[N x K]^T in bf16 (`part`: split-K
+// partials for small problems, may be null).
 hipError_t gemm_nt_bf16(const char* tag, const uint16_t* A, int64_t lda, const uint16_t* Bt, int64_t ldb, uint16_t* C, int64_t ldc,
-                        int64_t M, int64_t N, int64_t K, hipStream_t st) {
+                        int64_t M, int64_t N, int64_t K, hipStream_t st, float* part = nullptr) {
   GemmArgs g{};
   g.A = A; g.lda = lda; g.B = Bt; g.ldb = ldb; g.C = C; g.ldc = ldc;
   g.M = M; g.N = N; g.K = K; g.m_valid = M; g.ka_valid = K; g.kb_valid = K;
-  if (few_tiles(M, N, 256, N <= 128 ? 128 : 256)) return launch<CfgNTs<EPI_BF16, false>>(tag, g, 1, st);
+  if (few_tiles(M, N, 256, N <= 128 ? 128 : 256)) {
+    const SmallSplit p = part ? plan_small_split(M, N, K, 64) : SmallSplit{1, K};
+    if (p.splits > 1) {
+      g.C = part;
+      g.ldc = N;
+      g.k_split = p.k_split;
+      const hipError_t e = launch<CfgNTs<EPI_F32, false>>(tag, g, p.splits, st);
+      if (e != hipSuccess) return e;
+      return reduce_bf16(part, p.splits, M, N, C, ldc, st);
+    }
+    return launch<CfgNTs<EPI_BF16, false>>(tag, g, 1, st);
+  }
   if (N <= 128) return launch<CfgNT<128, EPI_BF16, false>>(tag, g, 1, st);
   return launch<CfgNT3>(tag, g, 1, st);
 }
@@ -314,26 +389,37 @@ hipError_t gemm_nt_bf16(const char* tag, const uint16_t* A, int64_t lda, const u
 // (2:4) products use stream-K instead: 256 workgroups with equal shares of
 // the tiles x K steps, each at least 8 steps.
 constexpr int kStreamWgs = 256;
+// Products that even split fill at most half the CUs with 256 x 256 tiles
+// (short K at small token counts) use 128 x 128 tiles and split-K only.
 struct SplitPlan {
   int splits;
   int64_t k_split;
   int64_t stream_steps;   // > 0: stream-K with this many K steps per tile
   int segs;               // stream-K partial tiles per workgroup
+  bool small;             // 128 x 128 tiles
 };
-SplitPlan plan_splits(int64_t M, int64_t N, int64_t K, bool allow_stream) {
-  if (K <= 0) return {0, 0, 0, 0};
-  const int64_t tiles = cdiv(M, 256) * cdiv(N, 256);
+SplitPlan plan_tiles(int64_t M, int64_t N, int64_t K, int tb) {
+  const int64_t tiles = cdiv(M, tb) * cdiv(N, tb);
   const int64_t steps = cdiv(K, 64);
   int64_t s = 256 / tiles;
   if (s < 1) s = 1;
   if (s > steps / 8) s = steps / 8 > 0 ? steps / 8 : 1;
   const int64_t k_split = cdiv(cdiv(K, s), 64) * 64;
-  const int splits = (int)cdiv(K, k_split);
-  if (allow_stream && tiles * splits * 10 < 9LL * kStreamWgs && tiles * steps >= 8LL * kStreamWgs) {
-    const int64_t longest = cdiv(tiles * steps, kStreamWgs);
-    return {1, K, steps, (int)((longest - 1) / steps + 2)};
+  return {(int)cdiv(K, k_split), k_split, 0, 0, tb == 128};
+}
+SplitPlan plan_splits(int64_t M, int64_t N, int64_t K, bool allow_stream) {
+  if (K <= 0) return {0, 0, 0, 0, false};
+  const SplitPlan big = plan_tiles(M, N, K, 256);
+  const int64_t tiles = cdiv(M, 256) * cdiv(N, 256), steps = cdiv(K, 64);
+  if (tiles * big.splits * 2 <= kStreamWgs) {
+    const SplitPlan sm = plan_tiles(M, N, K, 128);
+    if (cdiv(M, 128) * cdiv(N, 128) * sm.splits > 2 * tiles * big.splits) return sm;
   }
-  return {splits, k_split, 0, 0};
+  if (allow_stream && tiles * big.splits * 10 < 9LL * kStreamWgs && tiles * steps >= 8LL * kStreamWgs) {
+    const int64_t longest = cdiv(tiles * steps, kStreamWgs);
+    return {1, K, steps, (int)((longest - 1) / steps + 2), false};
+  }
+  return big;
 }
 size_t partial_bytes(int64_t M, int64_t N, int64_t K, bool allow_stream) {
   const SplitPlan p = plan_splits(M, N, K, allow_stream);
@@ -344,6 +430,9 @@ size_t partial_bytes(int64_t M, int64_t N, int64_t K, bool allow_stream) {
 // C = A^T B summed over K = T rows, reduced into out (optionally transposed),
 // keeping rows m < rows_out.  A is [K x M] dense (OP_T) or 2:4 compressed
 // along M (OP_TSP); B is [K x N] dense.
+template <int AMODE>
+using CfgTTs = GemmCfg<128, 128, 2, 2, AMODE, OP_T, EPI_F32, false>;
+
 template <int AMODE>
 hipError_t gemm_tt_f32(const char* tag, const uint16_t* A, int64_t lda, const uint8_t* Am, int64_t ldam, const uint16_t* B,
                        int64_t ldb, int64_t M, int64_t N, int64_t K, float* part, float* out, int64_t rows_out,
@@ -373,7 +462,7 @@ hipError_t gemm_tt_f32(const char* tag, const uint16_t* A, int64_t lda, const ui
                        g.tiles_n, (int64_t)g.tiles_m * g.tiles_n, N, rows_out, transpose ? 1 : 0, out, ldo);
     return hipGetLastError();
   }
-  hipError_t e = launch<Cfg>(tag, g, p.splits, st);
+  hipError_t e = p.small ? launch<CfgTTs<AMODE>>(tag, g, p.splits, st) : launch<Cfg>(tag, g, p.splits, st);
   if (e != hipSuccess) return e;
   TimedLaunch tl("splitk_reduce", st);
   hipLaunchKernelGGL(splitk_reduce_kernel, rgrid, dim3(256), 0, st, part, p.splits, M, N, rows_out,
@@ -383,9 +472,10 @@ hipError_t gemm_tt_f32(const char* tag, const uint16_t* A, int64_t lda, const ui
 
 struct FwdWs {
   uint16_t *U_upT, *V_upT, *U_downT, *V_downT;
+  float* part;   // split-K partials of the long-K products at small token counts
   size_t bytes;
 };
-FwdWs fwd_ws(char* p, int64_t d, int64_t F, int64_t r) {
+FwdWs fwd_ws(char* p, int64_t T, int64_t d, int64_t F, int64_t r) {
   const int64_t Fp = pad64(F);
   Carver c{p};
   FwdWs w;
@@ -393,6 +483,10 @@ FwdWs fwd_ws(char* p, int64_t d, int64_t F, int64_t r) {
   w.V_upT = c.take<uint16_t>(Fp * r);
   w.U_downT = c.take<uint16_t>(r * Fp);
   w.V_downT = c.take<uint16_t>(d * r);
+  size_t pb = small_split_bytes(T, r, d, 64);                 // k1
+  pb = std::max(pb, small_split_bytes(T, r, Fp, 64));          // k3 (2:4 or dense)
+  pb = std::max(pb, small_split_bytes(T, d, r, 64));           // k4
+  w.part = pb ? c.take<float>(pb / sizeof(float)) : nullptr;
   w.bytes = c.used;
   return w;
 }
@@ -423,6 +517,10 @@ BwdWs bwd_ws(char* p, int64_t T, int64_t d, int64_t F, int64_t r, bool dense, bo
   if (p2 > pb) pb = p2;
   if (p3 > pb) pb = p3;
   if (p4 > pb) pb = p4;
+  // split-K of the long-K bf16 products at small token counts (b1, b5, b8)
+  pb = std::max(pb, small_split_bytes(T, r, d, 64));
+  pb = std::max(pb, small_split_bytes(T, r, Fp, 64));
+  pb = std::max(pb, small_split_bytes(T, d, r, 64));
   w.part = c.take<float>(pb / sizeof(float));
   w.bytes = c.used;
   return w;
@@ -441,9 +539,8 @@ size_t spmm_workspace_bytes(int64_t K, int64_t N, int b_layout) {
 }
 
 size_t fwd_workspace_bytes(int64_t T, int64_t d, int64_t F, int64_t r, bool dense) {
-  (void)T;
   (void)dense;
-  return fwd_ws(nullptr, d, F, r).bytes;
+  return fwd_ws(nullptr, T, d, F, r).bytes;
 }
 
 size_t bwd_workspace_bytes(int64_t T, int64_t d, int64_t F, int64_t r, bool dense, bool ste) {
@@ -470,7 +567,7 @@ hipError_t run_spmm24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, 
 
 hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
   const int64_t T = a.T, d = a.d, F = a.F, r = a.r, Fp = pad64(F);
-  const FwdWs w = fwd_ws((char*)a.ws, d, F, r);
+  const FwdWs w = fwd_ws((char*)a.ws, T, d, F, r);
   // Weight factors laid out K-contiguous for the MFMA operands.
   Transposes tr;
   tr.add(a.U_up, d, r, r, w.U_upT, r, d, d);          // [r x d]
@@ -479,7 +576,7 @@ hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
   tr.add(a.V_down, r, d, d, w.V_downT, d, r, r);      // [d x r]
   ELAS_TRY(tr.launch(st));
   // P = x U_up
-  ELAS_TRY(gemm_nt_bf16("k1_up_gemm", a.x, d, w.U_upT, d, a.P, r, T, r, d, st));
+  ELAS_TRY(gemm_nt_bf16("k1_up_gemm", a.x, d, w.U_upT, d, a.P, r, T, r, d, st, w.part));
   if (!a.dense) {
     // H^T = V_up^T P^T with ReLU^2 + 2:4 selection + compression in the epilogue
     GemmArgs g{};
@@ -493,7 +590,7 @@ hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
     z.B = w.U_downT; z.ldb = Fp;
     z.M = T; z.N = r; z.K = Fp; z.m_valid = T; z.ka_valid = Fp; z.kb_valid = Fp;
     z.C = a.Z; z.ldc = r;
-    ELAS_TRY(launch_sp("k3_spmm_down", z, st));
+    ELAS_TRY(launch_sp("k3_spmm_down", z, st, w.part));
   } else {
     // dense activations: S = relu(H)^2 written [T x F], then a dense product
     GemmArgs g{};
@@ -501,10 +598,10 @@ hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
     g.M = Fp; g.N = T; g.K = r; g.m_valid = Fp; g.ka_valid = r; g.kb_valid = r;
     g.act = a.s_vals; g.ld_act = F; g.f_valid = F; g.act_square = 1;
     ELAS_TRY(launch_act<EPI_ACT_DENSE>("k2_up_relu2_dense", g, st));
-    ELAS_TRY(gemm_nt_bf16("k3_down_gemm_dense", a.s_vals, F, w.U_downT, Fp, a.Z, r, T, r, F, st));
+    ELAS_TRY(gemm_nt_bf16("k3_down_gemm_dense", a.s_vals, F, w.U_downT, Fp, a.Z, r, T, r, F, st, w.part));
   }
   // Y = Z V_down
-  ELAS_TRY(gemm_nt_bf16("k4_down_gemm", a.Z, r, w.V_downT, r, a.y, d, T, d, r, st));
+  ELAS_TRY(gemm_nt_bf16("k4_down_gemm", a.Z, r, w.V_downT, r, a.y, d, T, d, r, st, w.part));
   return hipSuccess;
 }
 
@@ -538,7 +635,7 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
   }
   const BwdWs w = bwd_ws((char*)a.ws, T, d, F, r, a.dense, a.ste);
   // dZ = dY V_down^T   (V_down [r x d] is already the K-contiguous operand)
-  ELAS_TRY(gemm_nt_bf16("b1_dZ", a.dy, d, a.V_down, d, w.dZ, r, T, r, d, st));
+  ELAS_TRY(gemm_nt_bf16("b1_dZ", a.dy, d, a.V_down, d, w.dZ, r, T, r, d, st, w.part));
   // dV_down = Z^T dY
   ELAS_TRY(gemm_tt_f32<OP_T>("b2_dV_down", a.Z, r, nullptr, 0, a.dy, d, r, d, T, w.part, a.dV_down, r, false, d, st));
   if (!a.dense && !a.ste) {
@@ -557,7 +654,7 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
     p.B = a.V_up; p.ldb = F;
     p.M = T; p.N = r; p.K = Fp; p.m_valid = T; p.ka_valid = Fp; p.kb_valid = F;
     p.C = w.dP; p.ldc = r;
-    ELAS_TRY(launch_sp("b5_spmm_dP", p, st));
+    ELAS_TRY(launch_sp("b5_spmm_dP", p, st, w.part));
     // dV_up = P^T dH, computed as dV_up^T = dH^T P and written transposed
     ELAS_TRY(gemm_tt_f32<OP_TSP>("b6_dV_up", w.dH, ldv, a.s_meta, ldm, a.P_in, r, Fp, r, T, w.part, a.dV_up, F, true, F,
                                  st));
@@ -591,7 +688,7 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
                                    F, false, r, st));
     }
     // dP = dH V_up^T (dense)
-    ELAS_TRY(gemm_nt_bf16("b5_dP_dense", w.dH, F, a.V_up, F, w.dP, r, T, r, F, st));
+    ELAS_TRY(gemm_nt_bf16("b5_dP_dense", w.dH, F, a.V_up, F, w.dP, r, T, r, F, st, w.part));
     // dV_up^T = dH^T P (dense), written transposed
     ELAS_TRY(gemm_tt_f32<OP_T>("b6_dV_up_dense", w.dH, F, nullptr, 0, a.P_in, r, F, r, T, w.part, a.dV_up, F, true,
                                F, st));
@@ -599,7 +696,7 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
   // dU_up = x^T dP
   ELAS_TRY(gemm_tt_f32<OP_T>("b7_dU_up", a.x, d, nullptr, 0, w.dP, r, d, r, T, w.part, a.dU_up, d, false, r, st));
   // dx = dP U_up^T   (U_up [d x r] is already K-contiguous)
-  ELAS_TRY(gemm_nt_bf16("b8_dx", w.dP, r, a.U_up, r, a.dx, d, T, d, r, st));
+  ELAS_TRY(gemm_nt_bf16("b8_dx", w.dP, r, a.U_up, r, a.dx, d, T, d, r, st, w.part));
   return hipSuccess;
 }
 

@@ -707,6 +707,22 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             }
           }
         }
+    } else if constexpr (Cfg::EPI == EPI_F32) {
+      // 2:4 products, split-K partial rows (layout as below): 32 lanes store
+      // 32 consecutive columns of one row per accumulator.
+      float* part = (float*)g.C + (int64_t)blockIdx.y * g.M * g.N;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int64_t col = n0 + wn * TN + j * 32 + lrow;
+          const int64_t row = m0 + wm * TM + i * 32 + lhalf * 4;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int dr = (e / 4) * 8 + (e % 4);
+            if (row + dr < g.M && col < g.N) part[(row + dr) * g.N + col] = acc[i][j][e];
+          }
+        }
     } else if constexpr (Cfg::EPI == EPI_BF16) {
       // 2:4 products (the sparse operand stays the MFMA's first): accumulator
       // 4b+q of lane l is C[row 8b + 4h + q][col l%32] of its 32x32 block.
