@@ -8,6 +8,8 @@ oracle (bf16 inputs, fp32 accumulation).
   weight gradients against the oracle with the same bf16 rounding points.
 * With exact small-integer inputs the fused ReLU^2 + 2:4 epilogue must
   match the oracle bit for bit (P, kept values, metadata).
+* Small token counts at the 1B shape exercise the split-K and 128 x 128 tile
+  paths in every activation mode.
 * Full-size workloads run in the benchmarked configuration and are checked
   on sampled tokens: every output row depends only on its own token, and the
   weight gradients are checked with dY zero outside the sampled tokens, so
@@ -195,6 +197,17 @@ def test_zero_tokens():
     torch.cuda.synchronize()
     for k in GRADS:
         assert torch.all(grads[k] == 0), k
+
+
+@pytest.mark.parametrize("mode", ["sparse", "dense", "ste"])
+@pytest.mark.parametrize("T", [256, 512])
+def test_small_token_counts_1b_shape(mode, T):
+    """The 1B shape at token counts where the long-K products split K over the
+    CUs (fp32 partials reduced to bf16) and the K = T products use 128 x 128
+    tiles: parity with the oracle in each activation mode."""
+    bits = config_inputs("llama1b", T=T, seed_base=60 + T)
+    f, b = offn.run(bits, sparse=(mode != "dense"), ste=(mode == "ste"))
+    compare(run_gpu(bits, mode=mode), f, b)
 
 
 @pytest.mark.parametrize("mode", ["dense", "ste"])
