@@ -153,7 +153,28 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   float4 acc[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) acc[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int k = 0; k < splits; ++k) {
+  // Splits are read four at a time (16 loads in flight per thread) and added
+  // in split order, so the result does not depend on the grouping.
+  int k = 0;
+  for (; k + 4 <= splits; k += 4) {
+    float4 v[4][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float* pk = part + (int64_t)(k + u) * M * N;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t m = m0 + ty + 16 * i;
+        v[u][i] = (m < rows_out && n < N) ? *(const float4*)(pk + m * N + n) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[i].x += v[u][i].x; acc[i].y += v[u][i].y; acc[i].z += v[u][i].z; acc[i].w += v[u][i].w;
+      }
+  }
+  for (; k < splits; ++k) {
     const float* pk = part + (int64_t)k * M * N;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -206,16 +227,28 @@ __global__ __launch_bounds__(256) void streamk_reduce_kernel(const float* __rest
   float4 acc[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) acc[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (; w < wgs; ++w) {
-    const int64_t b = beg_of(w), e = beg_of(w + 1);
-    if (b >= te) break;
-    if (e <= b) continue;
-    const float* slot = part + ((int64_t)w * segs + (t - b / S)) * 65536;
+  // The workgroups [w, w_end) that touch tile t, read four at a time (16
+  // loads in flight per thread) and added in workgroup order.
+  int64_t w_end = w;
+  while (w_end < wgs && beg_of(w_end) < te) ++w_end;
+  for (; w < w_end; w += 4) {
+    float4 v[4][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float4 v = *(const float4*)(slot + (int64_t)(lm + ty + 16 * i) * 256 + ln);
-      acc[i].x += v.x; acc[i].y += v.y; acc[i].z += v.z; acc[i].w += v.w;
+    for (int u = 0; u < 4; ++u) {
+      const int64_t wu = w + u;
+      const int64_t b = beg_of(wu), e = beg_of(wu + 1);
+      const bool has = wu < w_end && e > b;
+      const float* slot = part + ((int64_t)wu * segs + (t - b / S)) * 65536;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        v[u][i] = has ? *(const float4*)(slot + (int64_t)(lm + ty + 16 * i) * 256 + ln) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[i].x += v[u][i].x; acc[i].y += v[u][i].y; acc[i].z += v[u][i].z; acc[i].w += v[u][i].w;
+      }
   }
   reduce_store(acc, m0, n0, tx, ty, N, rows_out, transpose, out, ldo, tile);
 }
