@@ -1279,8 +1279,14 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           load_a(s + 1);
           issue_b(s + 1);
         }
-        compute(smem + buf * Cfg::STAGE, smem + buf * Cfg::STAGE + Cfg::A_PART, [](int) {});
-        if (more) sa.store(smem + (buf ^ 1) * Cfg::STAGE, tid);
+        // The expanded A of step s+1 is written to the other buffer (last
+        // read in step s-1, before the previous barrier) ahead of this step's
+        // last MFMA sub-step, so that its VALU work overlaps the MFMAs still
+        // in flight.  (Measured: 5 % faster than after the step; earlier
+        // sub-steps wait longer for A's loads or spill.)
+        compute(smem + buf * Cfg::STAGE, smem + buf * Cfg::STAGE + Cfg::A_PART, [&](int kk) {
+          if (kk == 3 && more) sa.store(smem + (buf ^ 1) * Cfg::STAGE, tid);
+        });
         wait_vmcnt<0>();   // B's DMA of step s+1 has landed
         __syncthreads();   // A's LDS writes and B's DMA of step s+1 are complete
       }
