@@ -455,7 +455,22 @@ def main() -> int:
         avg_s = ms / n / 1e3
         alg_bytes = M * N * (2 + 1.125)      # read bf16 h, write half the values + 2 bits each
         gbs = alg_bytes / avg_s / 1e9
+        # achievable-bandwidth context: a plain device copy of h's size (torch's copy kernel)
+        hc = torch.empty_like(h)
+        for _ in range(3):
+            hc.copy_(h)
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        c0.record()
+        for _ in range(20):
+            hc.copy_(h)
+        c1.record()
+        torch.cuda.synchronize()
+        copy_gbs = 2 * h.numel() * 2 / (c0.elapsed_time(c1) / 20 / 1e3) / 1e9
+        del hc
         result["sparsify"] = {"shape": [M, N], "avg_us": round(avg_s * 1e6, 2), "alg_bytes": alg_bytes,
+                              "copy_gbs_same_size": round(copy_gbs, 1),
+                              "frac_of_copy": round(gbs / copy_gbs, 4),
                               "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                               "frac": round(gbs / PEAK_HBM_GBS, 4)}
 
