@@ -474,6 +474,28 @@ def main() -> int:
                               "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                               "frac": round(gbs / PEAK_HBM_GBS, 4)}
 
+    # achievable-MFMA context: a large square bf16 GEMM through torch (hipBLASLt)
+    if not args.no_sparsify:
+        n_sq = 8192
+        a_sq = torch.randn(n_sq, n_sq, device=dev).to(bf)
+        b_sq = torch.randn(n_sq, n_sq, device=dev).to(bf)
+        c_sq = torch.empty(n_sq, n_sq, device=dev, dtype=bf)
+        for _ in range(3):
+            torch.matmul(a_sq, b_sq, out=c_sq)
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        g0.record()
+        for _ in range(10):
+            torch.matmul(a_sq, b_sq, out=c_sq)
+        g1.record()
+        torch.cuda.synchronize()
+        sq_tflops = 2.0 * n_sq ** 3 / (g0.elapsed_time(g1) / 10 / 1e3) / 1e12
+        result["mfma_achievable"] = {"gemm": f"bf16 {n_sq}^3, torch.matmul (hipBLASLt)",
+                                     "tflops": round(sq_tflops, 1), "frac_of_peak": round(sq_tflops / PEAK_BF16_TFLOPS, 4),
+                                     "dominant_kernel_frac_of_achievable": round(roofline["achieved"] / sq_tflops, 4)}
+        del a_sq, b_sq, c_sq
+        torch.cuda.empty_cache()
+
     if not args.no_large_batch and args.workload == "llama1b":
         print("[bench] large batch (T = 262144): compressed vs dense activations", file=sys.stderr, flush=True)
         torch.cuda.empty_cache()
