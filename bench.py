@@ -318,7 +318,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama1b")
-    ap.add_argument("--cpu-sample", type=int, default=16384, help="tokens for the CPU oracle baseline (0: skip)")
+    ap.add_argument("--cpu-sample", type=int, default=24576, help="tokens for the CPU oracle baseline (0: skip)")
     ap.add_argument("--no-sparsify", action="store_true", help="skip the standalone sparsify measurement")
     ap.add_argument("--no-large-batch", action="store_true",
                     help="skip the T = 262144 compressed-vs-dense activation comparison")

@@ -210,6 +210,15 @@ def test_small_token_counts_1b_shape(mode, T):
     compare(run_gpu(bits, mode=mode), f, b)
 
 
+@pytest.mark.parametrize("T,d,F,r", [(64, 64, 65536, 16), (40, 65536, 64, 8)])
+def test_maximum_widths(T, d, F, r):
+    """d_ff and d at the ABI's maximum (65536): 32 Ki kept values per row,
+    1024-step contractions, the long-K split of the forward and backward."""
+    bits = ffn_inputs(T, d, F, r, seed_base=7)
+    f, b = offn.run(bits)
+    compare(run_gpu(bits), f, b)
+
+
 @pytest.mark.parametrize("mode", ["dense", "ste"])
 @pytest.mark.parametrize("T,d,F,r", [(5, 16, 24, 8), (700, 136, 1000, 72), (300, 512, 1376, 128),
                                      (129, 2048, 5464, 512)])
