@@ -147,7 +147,9 @@ int elas_spmm_24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, int64
  * bf16 (nearest-even); every product accumulates in fp32.  The 2:4 selection
  * ranks max(0, bf16(H))^2 exactly, ties to the lower index.
  * flags: ELAS_MODE_SPARSE24 (0) or ELAS_MODE_DENSE.
- * workspace >= elas_lowrank_ffn_fwd_workspace_bytes(T, d, d_ff, r, flags).
+ * workspace >= elas_lowrank_ffn_fwd_workspace_bytes(T, d, d_ff, r, flags).  The
+ * size depends on T and is not monotonic in it (small token counts add fp32
+ * split-K partials), so query it for every T a buffer is reused for.
  * Requires T >= 0, d, d_ff, r > 0, multiples of 8 and at most 65536.  T == 0 is
  * a no-op (pointers are then not inspected and may be NULL).
  */
