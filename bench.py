@@ -187,11 +187,12 @@ TABLE3_PAPER = {
 def table3_compare(iters: int = 20, warmup: int = 3) -> dict:
     """Forward-only ELAS FFN (2:4 activations) vs the full-rank ReLU^2 FFN
     (elas_fullrank_ffn_fwd, dense MFMA) at the four model shapes and the token
-    counts of Table 3, as device time per call (see device_us).  The ELAS
-    entry point re-lays out its four weight factors on every call (one
-    launch of K-contiguous copies); `elas_weight_relayout_us` is that part of
-    its time.  The full-rank entry point takes its weights already
-    K-contiguous (linear-layer orientation).  `fullrank_hipblaslt_us` times
+    counts of Table 3, as device time per call (see device_us).  Both blocks
+    take their weights as a linear layer stores them (ELAS with
+    ELAS_FACTORS_AB: the A, B factors of Eq. 1), which is the kernels'
+    operand layout.  `elas_with_relayout_us` times the default ELAS call,
+    which re-lays out the four factors on every call (one launch;
+    `elas_weight_relayout_us` is that launch).  `fullrank_hipblaslt_us` times
     the same full-rank block built from torch.matmul (hipBLASLt) and torch
     elementwise kernels, as a reference for the baseline's quality."""
     import numpy as np
@@ -253,21 +254,27 @@ def table3_compare(iters: int = 20, warmup: int = 3) -> dict:
                 "Z": torch.empty((Tmax, r), dtype=bf, device=dev)}
         o_fr = {"y": torch.empty((Tmax, d), dtype=bf, device=dev), "S": torch.empty((Tmax, F), dtype=bf, device=dev)}
         # the workspace need is not monotonic in T (split-K partials at small T)
-        ws = torch.empty(max(1, *(elas.elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r) for T in TABLE3_SEQ)),
-                         dtype=torch.uint8, device=dev)
-        row = {"elas_us": [], "fullrank_us": [], "fullrank_hipblaslt_us": [], "speedup": [], "speedup_vs_best": []}
+        AB = elas.ELAS_FACTORS_AB
+        ws = torch.empty(max(1, *(elas.elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r, fl)
+                                  for T in TABLE3_SEQ for fl in (0, AB))), dtype=torch.uint8, device=dev)
+        fab = {n: t[n].t().contiguous() for n in ("U_up", "V_up", "U_down", "V_down")}
+        row = {"elas_us": [], "elas_with_relayout_us": [], "fullrank_us": [], "fullrank_hipblaslt_us": [],
+               "speedup": [], "speedup_vs_best": []}
         Wu_t, Wd_t = W_up.t(), W_down.t()
         for T in TABLE3_SEQ:
             x = t["x"][:T]
             ol = {n: v[:T] for n, v in o_lo.items()}
             of = {n: v[:T] for n, v in o_fr.items()}
-            e = device_us(lambda: elas.elas_lowrank_ffn_fwd(x, t["U_up"], t["V_up"], t["U_down"], t["V_down"],
-                                                            out=ol, workspace=ws))
+            e = device_us(lambda: elas.elas_lowrank_ffn_fwd(x, fab["U_up"], fab["V_up"], fab["U_down"], fab["V_down"],
+                                                            flags=AB, out=ol, workspace=ws))
+            e_rl = device_us(lambda: elas.elas_lowrank_ffn_fwd(x, t["U_up"], t["V_up"], t["U_down"], t["V_down"],
+                                                               out=ol, workspace=ws))
             f = device_us(lambda: elas.elas_fullrank_ffn_fwd(x, W_up, W_down, out=of))
             # the same block from the vendor GEMM library (torch.matmul -> hipBLASLt) and
             # torch elementwise kernels, as a reference for the full-rank time
             v = device_us(lambda: torch.matmul(torch.relu(torch.matmul(x, Wu_t)).square_(), Wd_t))
             row["elas_us"].append(round(e, 2))
+            row["elas_with_relayout_us"].append(round(e_rl, 2))
             row["fullrank_us"].append(round(f, 2))
             row["fullrank_hipblaslt_us"].append(round(v, 2))
             row["speedup"].append(round(f / e, 3))
@@ -287,7 +294,7 @@ def table3_compare(iters: int = 20, warmup: int = 3) -> dict:
         row["shape"] = {"d": d, "d_ff": F, "d_ff_true": c["d_ff_true"], "r": r}
         row["paper_speedup"] = TABLE3_PAPER[name]
         models[name] = row
-        del t, W_up, W_down, Wu_t, Wd_t, o_lo, o_fr, ws
+        del t, fab, W_up, W_down, Wu_t, Wd_t, o_lo, o_fr, ws
         torch.cuda.empty_cache()
     return {"seq": TABLE3_SEQ, "speedup_is": "fullrank_us / elas_us (forward only); speedup_vs_best uses the "
                                               "faster of fullrank_us and fullrank_hipblaslt_us",

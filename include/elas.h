@@ -80,6 +80,13 @@ extern "C" {
                                    (relu(h) recomputed from P and V_up); default is the
                                    masked derivative dH = dS * mask * 2 relu(h)               */
 
+/* elas_lowrank_ffn_fwd only: orientation of the four factors. */
+#define ELAS_FACTORS_AB      8u /* the factors are given as the A and B of Eq. 1 (W = A B, the
+                                   orientation a linear layer stores): U_up^T [r,d],
+                                   V_up^T [d_ff,r], U_down^T [r,d_ff], V_down^T [d,r].  This is
+                                   the kernels' operand layout, so nothing is re-laid out (for
+                                   inference with pre-arranged weights); results are identical */
+
 /* elas_spmm_24: layout of the dense operand B. */
 #define ELAS_B_KN            0  /* B is [K x N] row-major                         */
 #define ELAS_B_NK            1  /* B is [N x K] row-major (B^T stored)            */
@@ -146,7 +153,8 @@ int elas_spmm_24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, int64
  * Rounding points: P, H (before ReLU^2), the kept s, Z and y are rounded to
  * bf16 (nearest-even); every product accumulates in fp32.  The 2:4 selection
  * ranks max(0, bf16(H))^2 exactly, ties to the lower index.
- * flags: ELAS_MODE_SPARSE24 (0) or ELAS_MODE_DENSE.
+ * flags: ELAS_MODE_SPARSE24 (0) or ELAS_MODE_DENSE, optionally | ELAS_FACTORS_AB
+ *   (the four factor pointers then hold the transposed matrices listed there).
  * workspace >= elas_lowrank_ffn_fwd_workspace_bytes(T, d, d_ff, r, flags).  The
  * size depends on T and is not monotonic in it (small token counts add fp32
  * split-K partials), so query it for every T a buffer is reused for.

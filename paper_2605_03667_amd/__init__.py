@@ -20,10 +20,10 @@ import torch
 __all__ = [
     "ElasError", "lib", "elas_vals_ld", "elas_meta_ld", "elas_sparsify_24", "elas_spmm_24",
     "elas_spmm_24_workspace_bytes", "elas_lowrank_ffn_fwd", "elas_lowrank_ffn_fwd_workspace_bytes",
-    "elas_lowrank_ffn_bwd", "elas_lowrank_ffn_bwd_workspace_bytes",
+    "elas_lowrank_ffn_bwd", "elas_lowrank_ffn_bwd_workspace_bytes", "elas_fullrank_ffn_fwd",
     "elas_timing_enable", "elas_timing_collect",
     "ELAS_SPARSIFY_RELU2", "ELAS_SPARSIFY_RAW", "ELAS_B_KN", "ELAS_B_NK", "ELAS_MODE_SPARSE24",
-    "ELAS_MODE_DENSE", "ELAS_BWD_STE",
+    "ELAS_MODE_DENSE", "ELAS_BWD_STE", "ELAS_FACTORS_AB",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libelas.so")
@@ -35,6 +35,7 @@ ELAS_B_NK = 1
 ELAS_MODE_SPARSE24 = 0
 ELAS_MODE_DENSE = 2
 ELAS_BWD_STE = 4
+ELAS_FACTORS_AB = 8
 
 _STATUS = {0: "ELAS_OK", 1: "ELAS_ERR_NULL", 2: "ELAS_ERR_SHAPE", 3: "ELAS_ERR_ALIGN",
            4: "ELAS_ERR_WORKSPACE", 5: "ELAS_ERR_FLAGS", 6: "ELAS_ERR_DEVICE"}
@@ -174,10 +175,12 @@ def elas_lowrank_ffn_fwd(x, U_up, V_up, U_down, V_down, flags: int = 0, out: dic
     """Forward of the low-rank 2:4 FFN.  Returns dict(y, P, s_vals, s_meta, Z).
 
     With ``flags=ELAS_MODE_DENSE`` s_vals is the dense [T, d_ff] activation and
-    s_meta is None."""
+    s_meta is None.  With ``ELAS_FACTORS_AB`` the factors are passed transposed
+    (U_up^T [r, d], V_up^T [d_ff, r], U_down^T [r, d_ff], V_down^T [d, r])."""
     T, d = x.shape
-    r = U_up.shape[1]
-    F = V_up.shape[1]
+    ab = bool(flags & ELAS_FACTORS_AB)
+    r = U_up.shape[0] if ab else U_up.shape[1]
+    F = V_up.shape[0] if ab else V_up.shape[1]
     dev = x.device
     dense = bool(flags & ELAS_MODE_DENSE)
     if out is None:

@@ -131,7 +131,7 @@ int elas_spmm_24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, int64
 
 size_t elas_lowrank_ffn_fwd_workspace_bytes(int64_t T, int64_t d, int64_t d_ff, int64_t r, uint32_t flags) {
   if (T < 0 || d <= 0 || d_ff <= 0 || r <= 0) return 0;
-  return elas::fwd_workspace_bytes(T, d, d_ff, r, (flags & ELAS_MODE_DENSE) != 0);
+  return elas::fwd_workspace_bytes(T, d, d_ff, r, (flags & ELAS_MODE_DENSE) != 0, (flags & ELAS_FACTORS_AB) != 0);
 }
 
 int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t* V_up, const uint16_t* U_down,
@@ -139,8 +139,9 @@ int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t
                          uint16_t* y, uint16_t* P, uint16_t* s_vals, uint8_t* s_meta, uint16_t* Z,
                          void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
-  if (flags & ~ELAS_MODE_DENSE) return fail(ELAS_ERR_FLAGS, "forward flags: only ELAS_MODE_DENSE is allowed");
-  const bool dense = (flags & ELAS_MODE_DENSE) != 0;
+  if (flags & ~(ELAS_MODE_DENSE | ELAS_FACTORS_AB))
+    return fail(ELAS_ERR_FLAGS, "forward flags: only ELAS_MODE_DENSE and ELAS_FACTORS_AB are allowed");
+  const bool dense = (flags & ELAS_MODE_DENSE) != 0, ab = (flags & ELAS_FACTORS_AB) != 0;
   ELAS_CHECK(check_ffn_dims(T, d, d_ff, r));
   if (T == 0) return ELAS_OK;
   ELAS_CHECK(check_ptr(x, "x"));
@@ -153,7 +154,7 @@ int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t
   ELAS_CHECK(check_ptr(s_vals, "s_vals"));
   if (!dense) ELAS_CHECK(check_ptr(s_meta, "s_meta"));
   ELAS_CHECK(check_ptr(Z, "Z"));
-  const size_t need = elas::fwd_workspace_bytes(T, d, d_ff, r, dense);
+  const size_t need = elas::fwd_workspace_bytes(T, d, d_ff, r, dense, ab);
   if (workspace_bytes < need)
     return fail(ELAS_ERR_WORKSPACE, "workspace %zu bytes, %zu needed", workspace_bytes, need);
   if (need) ELAS_CHECK(check_ptr(workspace, "workspace"));
@@ -163,6 +164,7 @@ int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t
   a.y = y; a.P = P; a.P_in = P; a.s_vals = s_vals; a.s_meta = s_meta; a.Z = Z;
   a.ws = workspace;
   a.dense = dense;
+  a.ab = ab;
   return device_status(elas::run_fwd(a, (hipStream_t)stream), "forward launch");
 }
 

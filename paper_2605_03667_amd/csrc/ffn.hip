@@ -508,14 +508,17 @@ struct FwdWs {
   float* part;   // split-K partials of the long-K products at small token counts
   size_t bytes;
 };
-FwdWs fwd_ws(char* p, int64_t T, int64_t d, int64_t F, int64_t r) {
+// (ab: the caller passes the factors already K-contiguous; no copies)
+FwdWs fwd_ws(char* p, int64_t T, int64_t d, int64_t F, int64_t r, bool ab) {
   const int64_t Fp = pad64(F);
   Carver c{p};
-  FwdWs w;
-  w.U_upT = c.take<uint16_t>(r * d);
-  w.V_upT = c.take<uint16_t>(Fp * r);
-  w.U_downT = c.take<uint16_t>(r * Fp);
-  w.V_downT = c.take<uint16_t>(d * r);
+  FwdWs w{};
+  if (!ab) {
+    w.U_upT = c.take<uint16_t>(r * d);
+    w.V_upT = c.take<uint16_t>(Fp * r);
+    w.U_downT = c.take<uint16_t>(r * Fp);
+    w.V_downT = c.take<uint16_t>(d * r);
+  }
   size_t pb = small_split_bytes(T, r, d, 64);                 // k1
   pb = std::max(pb, small_split_bytes(T, r, Fp, 64));          // k3 (2:4 or dense)
   pb = std::max(pb, small_split_bytes(T, d, r, 64));           // k4
@@ -571,9 +574,9 @@ size_t spmm_workspace_bytes(int64_t K, int64_t N, int b_layout) {
   return b_layout == 0 ? align_up((size_t)K * N * sizeof(uint16_t)) : 0;
 }
 
-size_t fwd_workspace_bytes(int64_t T, int64_t d, int64_t F, int64_t r, bool dense) {
+size_t fwd_workspace_bytes(int64_t T, int64_t d, int64_t F, int64_t r, bool dense, bool ab) {
   (void)dense;
-  return fwd_ws(nullptr, T, d, F, r).bytes;
+  return fwd_ws(nullptr, T, d, F, r, ab).bytes;
 }
 
 size_t bwd_workspace_bytes(int64_t T, int64_t d, int64_t F, int64_t r, bool dense, bool ste) {
@@ -600,41 +603,50 @@ hipError_t run_spmm24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, 
 
 hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
   const int64_t T = a.T, d = a.d, F = a.F, r = a.r, Fp = pad64(F);
-  const FwdWs w = fwd_ws((char*)a.ws, T, d, F, r);
-  // Weight factors laid out K-contiguous for the MFMA operands.
-  Transposes tr;
-  tr.add(a.U_up, d, r, r, w.U_upT, r, d, d);          // [r x d]
-  tr.add(a.V_up, r, F, F, w.V_upT, Fp, r, r);         // [Fp x r], zero rows >= F
-  tr.add(a.U_down, F, r, r, w.U_downT, r, Fp, Fp);    // [r x Fp], zero cols >= F
-  tr.add(a.V_down, r, d, d, w.V_downT, d, r, r);      // [d x r]
-  ELAS_TRY(tr.launch(st));
+  const FwdWs w = fwd_ws((char*)a.ws, T, d, F, r, a.ab);
+  // Weight factors K-contiguous for the MFMA operands: laid out here, or
+  // given so (ELAS_FACTORS_AB: unpadded d_ff, whose missing rows / columns
+  // the loads read as zero, exactly like the zero padding of the copies).
+  const uint16_t *U_upT = a.U_up, *V_upT = a.V_up, *U_downT = a.U_down, *V_downT = a.V_down;
+  int64_t F_rows = F, ld_ud = F;   // rows of V_up^T, pitch (= K extent) of U_down^T
+  if (!a.ab) {
+    Transposes tr;
+    tr.add(a.U_up, d, r, r, w.U_upT, r, d, d);          // [r x d]
+    tr.add(a.V_up, r, F, F, w.V_upT, Fp, r, r);         // [Fp x r], zero rows >= F
+    tr.add(a.U_down, F, r, r, w.U_downT, r, Fp, Fp);    // [r x Fp], zero cols >= F
+    tr.add(a.V_down, r, d, d, w.V_downT, d, r, r);      // [d x r]
+    ELAS_TRY(tr.launch(st));
+    U_upT = w.U_upT; V_upT = w.V_upT; U_downT = w.U_downT; V_downT = w.V_downT;
+    F_rows = Fp;
+    ld_ud = Fp;
+  }
   // P = x U_up
-  ELAS_TRY(gemm_nt_bf16("k1_up_gemm", a.x, d, w.U_upT, d, a.P, r, T, r, d, st, w.part));
+  ELAS_TRY(gemm_nt_bf16("k1_up_gemm", a.x, d, U_upT, d, a.P, r, T, r, d, st, w.part));
   if (!a.dense) {
     // H^T = V_up^T P^T with ReLU^2 + 2:4 selection + compression in the epilogue
     GemmArgs g{};
-    g.A = w.V_upT; g.lda = r; g.B = a.P; g.ldb = r;
-    g.M = Fp; g.N = T; g.K = r; g.m_valid = Fp; g.ka_valid = r; g.kb_valid = r;
+    g.A = V_upT; g.lda = r; g.B = a.P; g.ldb = r;
+    g.M = Fp; g.N = T; g.K = r; g.m_valid = F_rows; g.ka_valid = r; g.kb_valid = r;
     g.sv = a.s_vals; g.sm = a.s_meta; g.ldv = vals_ld(F); g.ldm = meta_ld(F);
     ELAS_TRY(launch_staged<EPI_SPARSIFY>("k2_up_relu2_sparsify", g, st));
     // Z = S U_down on the 2:4 operand
     GemmArgs z{};
     z.A = a.s_vals; z.lda = vals_ld(F); z.Am = a.s_meta; z.ldam = meta_ld(F);
-    z.B = w.U_downT; z.ldb = Fp;
-    z.M = T; z.N = r; z.K = Fp; z.m_valid = T; z.ka_valid = Fp; z.kb_valid = Fp;
+    z.B = U_downT; z.ldb = ld_ud;
+    z.M = T; z.N = r; z.K = Fp; z.m_valid = T; z.ka_valid = Fp; z.kb_valid = ld_ud;
     z.C = a.Z; z.ldc = r;
     ELAS_TRY(launch_sp("k3_spmm_down", z, st, w.part));
   } else {
     // dense activations: S = relu(H)^2 written [T x F], then a dense product
     GemmArgs g{};
-    g.A = w.V_upT; g.lda = r; g.B = a.P; g.ldb = r;
-    g.M = Fp; g.N = T; g.K = r; g.m_valid = Fp; g.ka_valid = r; g.kb_valid = r;
+    g.A = V_upT; g.lda = r; g.B = a.P; g.ldb = r;
+    g.M = Fp; g.N = T; g.K = r; g.m_valid = F_rows; g.ka_valid = r; g.kb_valid = r;
     g.act = a.s_vals; g.ld_act = F; g.f_valid = F; g.act_square = 1;
     ELAS_TRY(launch_act<EPI_ACT_DENSE>("k2_up_relu2_dense", g, st));
-    ELAS_TRY(gemm_nt_bf16("k3_down_gemm_dense", a.s_vals, F, w.U_downT, Fp, a.Z, r, T, r, F, st, w.part));
+    ELAS_TRY(gemm_nt_bf16("k3_down_gemm_dense", a.s_vals, F, U_downT, ld_ud, a.Z, r, T, r, F, st, w.part));
   }
   // Y = Z V_down
-  ELAS_TRY(gemm_nt_bf16("k4_down_gemm", a.Z, r, w.V_downT, r, a.y, d, T, d, r, st, w.part));
+  ELAS_TRY(gemm_nt_bf16("k4_down_gemm", a.Z, r, V_downT, r, a.y, d, T, d, r, st, w.part));
   return hipSuccess;
 }
 

@@ -50,11 +50,12 @@ struct FfnArgs {
   void* ws;
   bool dense;   // activations dense [T x d_ff] (no 2:4 selection)
   bool ste;     // backward: straight-through estimator through the selection
+  bool ab;      // forward: factors given as U_up^T, V_up^T, U_down^T, V_down^T
 };
 
 // ffn.hip
 size_t spmm_workspace_bytes(int64_t K, int64_t N, int b_layout);
-size_t fwd_workspace_bytes(int64_t T, int64_t d, int64_t F, int64_t r, bool dense);
+size_t fwd_workspace_bytes(int64_t T, int64_t d, int64_t F, int64_t r, bool dense, bool ab);
 size_t bwd_workspace_bytes(int64_t T, int64_t d, int64_t F, int64_t r, bool dense, bool ste);
 hipError_t run_spmm24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, int64_t K,
                       const uint16_t* b, int64_t N, bool b_is_nk, uint16_t* c, void* ws,

@@ -45,6 +45,7 @@ def test_binding_constants_match_header():
     assert d["ELAS_B_KN"] == elas.ELAS_B_KN and d["ELAS_B_NK"] == elas.ELAS_B_NK
     assert d["ELAS_MODE_SPARSE24"] == elas.ELAS_MODE_SPARSE24 and d["ELAS_MODE_DENSE"] == elas.ELAS_MODE_DENSE
     assert d["ELAS_BWD_STE"] == elas.ELAS_BWD_STE
+    assert d["ELAS_FACTORS_AB"] == elas.ELAS_FACTORS_AB
     for k, v in elas._STATUS.items():
         assert d[v] == k
 
@@ -107,6 +108,10 @@ def test_fwd_validation():
     L = elas.lib()
     assert _fwd(L, flags=1) == 5
     assert _fwd(L, flags=4) == 5                # STE is a backward-only flag
+    assert _fwd(L, flags=16) == 5
+    # pre-arranged factors need no factor copies in the workspace
+    assert (L.elas_lowrank_ffn_fwd_workspace_bytes(65536, 2048, 5464, 512, 8)
+            < L.elas_lowrank_ffn_fwd_workspace_bytes(65536, 2048, 5464, 512, 0))
     assert _fwd(L, d=12) == 2
     assert _fwd(L, F=60) == 2
     assert _fwd(L, r=0) == 2

@@ -210,6 +210,28 @@ def test_small_token_counts_1b_shape(mode, T):
     compare(run_gpu(bits, mode=mode), f, b)
 
 
+@pytest.mark.parametrize("dense", [False, True])
+@pytest.mark.parametrize("T,d,F,r,cfg", [(700, 136, 1000, 72, None), (1024, 2048, 5464, 512, "llama1b"),
+                                         (256, 2048, 5464, 512, "llama1b")])
+def test_factors_ab_identical(T, d, F, r, cfg, dense):
+    """ELAS_FACTORS_AB (factors passed as the A, B of Eq. 1, i.e. transposed)
+    reads the same operands as the copies the default forward makes, with the
+    unpadded d_ff read as zero beyond its end: every output is bit-identical."""
+    bits = config_inputs(cfg, T=T) if cfg else ffn_inputs(T, d, F, r, seed_base=3)
+    t = {k: dev_bf16(v) for k, v in bits.items()}
+    mode = elas.ELAS_MODE_DENSE if dense else 0
+    ref = elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], flags=mode)
+    tr = {k: t[k].t().contiguous() for k in ("U_up", "V_up", "U_down", "V_down")}
+    got = elas.elas_lowrank_ffn_fwd(t["x"], tr["U_up"], tr["V_up"], tr["U_down"], tr["V_down"],
+                                    flags=mode | elas.ELAS_FACTORS_AB)
+    torch.cuda.synchronize()
+    for k in ("y", "P", "s_vals", "s_meta", "Z"):
+        if ref[k] is None:
+            continue
+        assert torch.equal(ref[k].view(torch.int16) if ref[k].dtype == torch.bfloat16 else ref[k],
+                           got[k].view(torch.int16) if got[k].dtype == torch.bfloat16 else got[k]), k
+
+
 @pytest.mark.parametrize("T,d,F,r", [(64, 64, 65536, 16), (40, 65536, 64, 8)])
 def test_maximum_widths(T, d, F, r):
     """d_ff and d at the ABI's maximum (65536): 32 Ki kept values per row,
