@@ -1,0 +1,60 @@
+"""The entry points are capture-safe: a forward + backward captured in a HIP
+graph (torch.cuda.CUDAGraph) and replayed several times, with eager work and
+synchronisations between the replays, reproduces the eager results bit for
+bit (the library allocates nothing and enqueues only kernels on the caller's
+stream)."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2605_03667_amd as elas
+from synthetic import config_inputs, ffn_inputs
+from tests.helpers import dev_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("name,T", [(None, 300), ("llama1b", 512)])
+@pytest.mark.parametrize("mode", ["sparse", "dense", "ste"])
+def test_graph_replays_match_eager(name, T, mode):
+    bits = config_inputs(name, T=T) if name else ffn_inputs(T, 128, 264, 32, seed_base=9)
+    t = {k: dev_bf16(v) for k, v in bits.items()}
+    T, d = bits["x"].shape
+    r, F = bits["V_up"].shape
+    fflags = elas.ELAS_MODE_DENSE if mode == "dense" else 0
+    bflags = {"sparse": 0, "ste": elas.ELAS_BWD_STE, "dense": elas.ELAS_MODE_DENSE}[mode]
+    saved = elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], flags=fflags)
+    grads = elas.elas_lowrank_ffn_bwd(t["dY"], t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], saved,
+                                      flags=bflags)
+    wsf = torch.empty(max(1, elas.elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r, fflags)), dtype=torch.uint8,
+                      device="cuda:0")
+    wsb = torch.empty(max(1, elas.elas_lowrank_ffn_bwd_workspace_bytes(T, d, F, r, bflags)), dtype=torch.uint8,
+                      device="cuda:0")
+
+    def step():
+        elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], flags=fflags, out=saved,
+                                  workspace=wsf)
+        elas.elas_lowrank_ffn_bwd(t["dY"], t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], saved,
+                                  flags=bflags, grads=grads, workspace=wsb)
+
+    step()
+    torch.cuda.synchronize()
+    outs = {k: v for k, v in list(saved.items()) + list(grads.items()) if v is not None}
+    ref = {k: v.clone() for k, v in outs.items()}
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for rep in range(3):
+        for v in outs.values():
+            v.zero_()                     # eager work between the replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for k, v in outs.items():
+            assert torch.equal(v, ref[k]), (rep, k)
