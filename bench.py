@@ -337,7 +337,8 @@ def main() -> int:
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (--gpus {args.gpus} requested): the ELAS FFN path here is "
-              f"single-GPU; see DESIGN.md for how it would shard.", file=sys.stderr)
+              f"single-GPU (data parallelism over tokens would add one all-reduce of the four weight "
+              f"gradients per step, not built).", file=sys.stderr)
         return 2
 
     import numpy as np
