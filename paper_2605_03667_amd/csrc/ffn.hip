@@ -3,6 +3,7 @@
 // the standalone 2:4 sparse x dense product.  Everything runs on the caller's
 // stream in the caller's workspace; nothing here allocates.
 #include <algorithm>
+#include <atomic>
 
 #include "gemm.h"
 #include "internal.h"
@@ -290,16 +291,17 @@ template <int AMODE>
 using CfgTT = GemmCfg<256, 256, 4, 2, AMODE, OP_T, EPI_F32, false>;
 
 // Compute units of the current device (cached per device id).
+// (Relaxed atomics: concurrent first calls store the same value.)
 int device_cus() {
-  static int cached[64] = {0};
+  static std::atomic<int> cached[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
-    int n = 0;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cached[dev] = n;
+    cached[dev].store(n, std::memory_order_relaxed);
   }
-  return cached[dev];
+  return n;
 }
 
 template <class Cfg>
