@@ -382,9 +382,13 @@ hipError_t launch_sp(const char* tag, GemmArgs g, hipStream_t st, float* part = 
   return launch<CfgSP>(tag, g, 1, st);
 }
 // Epilogues that select and compress 2:4 groups (features along M).
+// With more than 3 MB of A rows (the d_ff-wide weight factor: 5.6 MB at 1B,
+// beyond an XCD's 4 MB L2) and an even number of 256-row tiles, two panels.
 template <int EPI>
-hipError_t launch_staged(const char* tag, const GemmArgs& g, hipStream_t st) {
+hipError_t launch_staged(const char* tag, GemmArgs g, hipStream_t st) {
   if (few_tiles(g.M, g.N, 256, 256)) return launch<CfgNT<128, EPI, true>>(tag, g, 1, st);
+  const int64_t tiles_m = cdiv(g.M, 256);
+  if (tiles_m % 2 == 0 && tiles_m * 256 * g.K * 2 > (int64_t(3) << 20)) g.m_groups = 2;
   return launch<CfgNT<256, EPI, true>>(tag, g, 1, st);
 }
 // Epilogues that write or read the dense activation (features along M).

@@ -88,6 +88,10 @@ struct GemmArgs {
   int64_t f_valid;
   int act_square;
   int tiles_m, tiles_n;
+  // M-fast direct kernels: when > 1, the XCDs split the M tiles into this many
+  // contiguous panels (XCD x takes panel x % m_groups and a share of the N
+  // tiles), so that the A rows a panel needs stay resident in the XCD's L2.
+  int m_groups;
   // Stream-K (register-staged path, EPI_F32): when stream_steps > 0, the
   // gridDim.x workgroups split the tiles x stream_steps K steps into equal
   // contiguous ranges; workgroup w writes the partial tile of the j-th tile
@@ -526,9 +530,26 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
   const int64_t kend = kbeg + g.k_split < g.K ? kbeg + g.k_split : g.K;
   const int nsteps = kend > kbeg ? (int)((kend - kbeg + BK - 1) / BK) : 0;
   const int lrow = lane & 31, lhalf = lane >> 5;
+  // Panel of this workgroup's XCD (m_groups > 1): M tiles [pm_begin, +pm_count),
+  // N tiles from pn_begin; tiles are then numbered locally, M fastest.
+  const bool panels = Cfg::M_FAST && g.m_groups > 1 && gridDim.x % 8 == 0 && 8 % g.m_groups == 0;
+  int pm_begin = 0, pm_count = g.tiles_m, pn_begin = 0, pn_count = g.tiles_n;
+  if (panels) {
+    const int x = blockIdx.x % 8, per = 8 / g.m_groups, gi = x % g.m_groups, xi = x / g.m_groups;
+    pm_begin = gi * g.tiles_m / g.m_groups;
+    pm_count = (gi + 1) * g.tiles_m / g.m_groups - pm_begin;
+    pn_begin = xi * g.tiles_n / per;
+    pn_count = (xi + 1) * g.tiles_n / per - pn_begin;
+  }
   auto origin = [&](int tile, int64_t& m0, int64_t& n0) __attribute__((always_inline)) {
-    const int tm = Cfg::M_FAST ? tile % g.tiles_m : tile / g.tiles_n;
-    const int tn = Cfg::M_FAST ? tile / g.tiles_m : tile % g.tiles_n;
+    int tm, tn;
+    if (panels) {
+      tm = pm_begin + tile % pm_count;
+      tn = pn_begin + tile / pm_count;
+    } else {
+      tm = Cfg::M_FAST ? tile % g.tiles_m : tile / g.tiles_n;
+      tn = Cfg::M_FAST ? tile / g.tiles_m : tile % g.tiles_n;
+    }
     m0 = (int64_t)tm * BM;
     n0 = (int64_t)tn * BN;
   };
@@ -1013,7 +1034,8 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     // current tile's step 0); the loads issued ahead run on into the next
     // tile, so its first loads are in flight during this tile's last steps
     // and epilogue.
-    const TileRange tr = tile_range(blockIdx.x, gridDim.x, ntiles);
+    const TileRange tr = panels ? TileRange{(int)blockIdx.x / 8, (int)gridDim.x / 8, pm_count * pn_count}
+                                : tile_range(blockIdx.x, gridDim.x, ntiles);
     if (tr.first >= tr.end) return;
     int tile = tr.first;
     int64_t m0, n0;
