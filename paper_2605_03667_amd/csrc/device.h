@@ -13,6 +13,7 @@ typedef __bf16 bf16x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // float -> bf16 bits, round to nearest, ties to even.  Integer formulation:
 // adding 0x7FFF plus the lowest kept bit carries into the kept half exactly

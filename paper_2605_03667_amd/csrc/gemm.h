@@ -950,7 +950,10 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         const int q = it * NT + tid, row = q / (BM / 16), c = q % (BM / 16);
         if (row < t_end && c * 16 < f_end) {
           const uint32_t* sp = (const uint32_t*)(lv + row * BM + (c ^ (row & 15)) * 16);
-          *(uint4*)(dst + (n0 + row) * g.ldv + m0 / 2 + c * 8) = make_uint4(sp[0], sp[1], sp[2], sp[3]);
+          // non-temporal: the compressed rows stream out and should not evict
+          // the weight panel this XCD keeps in L2
+          const u32x4 v = {sp[0], sp[1], sp[2], sp[3]};
+          __builtin_nontemporal_store(v, (u32x4*)(dst + (n0 + row) * g.ldv + m0 / 2 + c * 8));
         }
       }
       if constexpr (Cfg::EPI == EPI_SPARSIFY) {
@@ -960,7 +963,8 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           const int q = it * NT + tid, row = q / (BM / 64), c = q % (BM / 64);
           if (q < MCH && row < t_end && c * 64 < f_end) {
             const uint32_t* sp = (const uint32_t*)(lm + row * MP + c * 8);
-            *(uint2*)(g.sm + (n0 + row) * g.ldm + m0 / 8 + c * 8) = make_uint2(sp[0], sp[1]);
+            const u32x2 v = {sp[0], sp[1]};
+            __builtin_nontemporal_store(v, (u32x2*)(g.sm + (n0 + row) * g.ldm + m0 / 8 + c * 8));
           }
         }
       }
