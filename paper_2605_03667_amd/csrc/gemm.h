@@ -251,6 +251,24 @@ __device__ __forceinline__ void dma_b32_s(const void* sbase, uint32_t voff, uint
                "s"(__builtin_amdgcn_readfirstlane(lds_wave_base))
                : "memory", "m0");
 }
+// Non-temporal forms (nt: streamed data that is read once and should not
+// displace what a workgroup keeps in L2).
+__device__ __forceinline__ void dma_b128_nt(const void* g, uint32_t lds_wave_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt" ::"v"(g), "s"(lds_wave_base) : "memory", "m0");
+}
+__device__ __forceinline__ void dma_b32_nt(const void* g, uint32_t lds_wave_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off nt" ::"v"(g), "s"(lds_wave_base) : "memory", "m0");
+}
+__device__ __forceinline__ void dma_b128_nt_s(const void* sbase, uint32_t voff, uint32_t lds_wave_base) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 nt" ::"v"(voff), "s"(uniform_ptr(sbase)),
+               "s"(__builtin_amdgcn_readfirstlane(lds_wave_base))
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma_b32_nt_s(const void* sbase, uint32_t voff, uint32_t lds_wave_base) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1 nt" ::"v"(voff), "s"(uniform_ptr(sbase)),
+               "s"(__builtin_amdgcn_readfirstlane(lds_wave_base))
+               : "memory", "m0");
+}
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
@@ -1144,15 +1162,15 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
               const int blk = wave * VPW + j;
               const int b = blk * 1024 + lane * 16;
               const int row = b / BM, c = ((b % BM) / 16) ^ (row & 15);
-              dma_b128_s(vbase, (uint32_t)row * (uint32_t)(g.ldv * 2) + (uint32_t)c * 16u, smem_lds + off + blk * 1024);
+              dma_b128_nt_s(vbase, (uint32_t)row * (uint32_t)(g.ldv * 2) + (uint32_t)c * 16u, smem_lds + off + blk * 1024);
             }
 #pragma unroll
             for (int j = 0; j < MPW; ++j) {
               const int blk = wave * MPW + j;
               const int q = blk * 64 + lane, row = q / MPD, w = q % MPD;
               const bool real = row < BN && w < MPD - 1;
-              dma_b32_s(mbase, real ? (uint32_t)row * (uint32_t)g.ldm + 4u * (uint32_t)w : 0u,
-                        smem_lds + lm_off + blk * 256);
+              dma_b32_nt_s(mbase, real ? (uint32_t)row * (uint32_t)g.ldm + 4u * (uint32_t)w : 0u,
+                           smem_lds + lm_off + blk * 256);
             }
           } else {
             // edge tile: checked addresses (lane index laundered so that they
@@ -1166,7 +1184,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
               const int row = b / BM, c = ((b % BM) / 16) ^ (row & 15);
               const void* src = (row < t_end && c * 16 < f_end) ? (const void*)(g.sv + (tn0 + row) * g.ldv + tm0 / 2 + c * 8)
                                                                 : (const void*)g_dma_zero;
-              dma_b128(src, __builtin_amdgcn_readfirstlane(smem_lds + off + blk * 1024));
+              dma_b128_nt(src, __builtin_amdgcn_readfirstlane(smem_lds + off + blk * 1024));
             }
 #pragma unroll
             for (int j = 0; j < MPW; ++j) {
@@ -1175,7 +1193,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
               const void* src = (row < BN && row < t_end && w < MPD - 1 && 32 * w < f_end)
                                     ? (const void*)(g.sm + (tn0 + row) * g.ldm + tm0 / 8 + 4 * w)
                                     : (const void*)g_dma_zero;
-              dma_b32(src, __builtin_amdgcn_readfirstlane(smem_lds + lm_off + blk * 256));
+              dma_b32_nt(src, __builtin_amdgcn_readfirstlane(smem_lds + lm_off + blk * 256));
             }
           }
         }
