@@ -97,6 +97,44 @@ __device__ __forceinline__ uint32_t top2_code_of(const Top2& t) {
   return 15u - ((t.first >> 30) | ((t.second >> 30) << 2));
 }
 
+// relu of an fp32 value with NaN sent to 0: v_max_f32 returns the non-NaN
+// operand.  Written as one instruction because the compiler's fmaxf first
+// quiets its input (a second instruction).
+__device__ __forceinline__ float relu_f32(float x) {
+  float r;
+  asm("v_max_f32 %0, 0, %1" : "=v"(r) : "v"(x));
+  return r;
+}
+
+// The same top-2 as top2_keys, for the fused epilogues, with fewer
+// instructions.  The inputs hold non-negative bf16 pairs (p01 = r0 | r1 << 16,
+// p23 = r2 | r3 << 16).  Key of element i: r << 16 | (3 - i), built with one
+// instruction each.  With m and e the largest and middle key of elements
+// 0..2, the largest of all four is max(m, k3) and the second largest
+// max(e, min(m, k3)).  Rotating right by 2 moves the index bits to the top
+// (r sits at bits 14..29, bits 0..13 are zero), which orders the kept pair by
+// index; `first << 2` and `second << 2` are the kept values as fp32.
+__device__ __forceinline__ Top2 top2_keys_hi(uint32_t p01, uint32_t p23) {
+  const uint32_t k0 = (p01 << 16) | 3u;
+  const uint32_t k1 = (p01 & 0xFFFF0000u) | 2u;
+  const uint32_t k2 = (p23 << 16) | 1u;
+  const uint32_t k3 = p23 & 0xFFFF0000u;
+  uint32_t m, e;   // v_max3_u32 / v_med3_u32 (not formed from min/max by the compiler)
+  asm("v_max3_u32 %0, %1, %2, %3" : "=v"(m) : "v"(k0), "v"(k1), "v"(k2));
+  asm("v_med3_u32 %0, %1, %2, %3" : "=v"(e) : "v"(k0), "v"(k1), "v"(k2));
+  const uint32_t t1 = __builtin_elementwise_max(m, k3);
+  const uint32_t t2 = __builtin_elementwise_max(e, __builtin_elementwise_min(m, k3));
+  const uint32_t r1 = __builtin_amdgcn_alignbit(t1, t1, 2), r2 = __builtin_amdgcn_alignbit(t2, t2, 2);
+  Top2 t;
+  t.first = __builtin_elementwise_max(r1, r2);
+  t.second = __builtin_elementwise_min(r1, r2);
+  return t;
+}
+// (3 - i0) | (3 - i1) << 2 of a top2_keys_hi result: the code XOR 15.
+__device__ __forceinline__ uint32_t top2_code_xor15(const Top2& t) {
+  return (t.first >> 30) | ((t.second >> 28) & 0xCu);
+}
+
 // Square root rounded to bf16 for a non-negative bf16 value s given as fp32.
 // The raw v_sqrt_f32 result rounds to the same bf16 as the correctly rounded
 // square root for every such s with a normal exponent (checked over all bf16

@@ -914,15 +914,18 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             uint32_t codes = 0;   // code of group b at bits 8b .. 8b+3
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
-              // h rounded to bf16 (RNE), relu'd, ranked (ties to the lower index)
-              const uint32_t p01 = relu_bits2(bf16x2_rne(acc[i][j][4 * b], acc[i][j][4 * b + 1]));
-              const uint32_t p23 = relu_bits2(bf16x2_rne(acc[i][j][4 * b + 2], acc[i][j][4 * b + 3]));
-              const Top2 t = top2_keys(p01, p23);
-              codes |= top2_code_of(t) << (8 * b);
-              const float a = __builtin_bit_cast(float, t.first << 16);
-              const float c = __builtin_bit_cast(float, t.second << 16);
+              // h relu'd and rounded to bf16 (RNE; the same bits as rounding
+              // first, as the rounding keeps the sign), ranked (ties to the
+              // lower index)
+              const uint32_t p01 = bf16x2_rne(relu_f32(acc[i][j][4 * b]), relu_f32(acc[i][j][4 * b + 1]));
+              const uint32_t p23 = bf16x2_rne(relu_f32(acc[i][j][4 * b + 2]), relu_f32(acc[i][j][4 * b + 3]));
+              const Top2 t = top2_keys_hi(p01, p23);
+              codes |= top2_code_xor15(t) << (8 * b);
+              const float a = __builtin_bit_cast(float, t.first << 2);
+              const float c = __builtin_bit_cast(float, t.second << 2);
               pair[b] = bf16x2_rne(a * a, c * c);   // s = relu(h)^2 of the kept pair, index order
             }
+            codes ^= 0x0F0F0F0Fu;
             // metadata byte b = code of group 2b (lane half 0) | code of group
             // 2b+1 (half 1) << 4; the swap hands half 0 its partner's codes
             const uint32_t other_codes = __builtin_amdgcn_permlane32_swap(codes, codes, false, false)[1];
@@ -936,24 +939,42 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             // EPI_DH: scale dS at the kept positions of the stored group by
             // 2 relu(h), relu(h) = bf16(sqrt(s)) exactly; result in place.
             if (ok) {
-              const uint32_t word = *(const uint32_t*)(lm + tl * MP + fl / 8);
+              // group b's code at bits 8b .. 8b+3
+              const uint32_t w = *(const uint32_t*)(lm + tl * MP + fl / 8) >> (4 * lhalf);
+              uint32_t* loc[4];
+              float s[4][2], rt[4][2];
+              bool tiny = false;   // a subnormal s (the raw square root flushes it)
 #pragma unroll
               for (int b = 0; b < 4; ++b) {
-                uint32_t* loc = (uint32_t*)(lv + val_word(tl, fl / 4 + 2 * b + lhalf));
-                const uint32_t sv = *loc;
-                const uint32_t code = (word >> (8 * b + 4 * lhalf)) & 0xFu;
-                const uint32_t i0 = code & 3u, i1 = code >> 2;
+                loc[b] = (uint32_t*)(lv + val_word(tl, fl / 4 + 2 * b + lhalf));
+                const uint32_t sv = *loc[b];
+                s[b][0] = __builtin_bit_cast(float, sv << 16);
+                s[b][1] = __builtin_bit_cast(float, sv & 0xFFFF0000u);
+                tiny |= __builtin_amdgcn_classf(s[b][0], 0x80) | __builtin_amdgcn_classf(s[b][1], 0x80);
+              }
+              if (__builtin_amdgcn_ballot_w64(tiny) == 0) {
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+#pragma unroll
+                  for (int e = 0; e < 2; ++e) rt[b][e] = __builtin_amdgcn_sqrtf(s[b][e]);
+              } else {
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+#pragma unroll
+                  for (int e = 0; e < 2; ++e) rt[b][e] = sqrt_for_bf16(s[b][e]);
+              }
+#pragma unroll
+              for (int b = 0; b < 4; ++b) {
+                const uint32_t i0 = __builtin_amdgcn_ubfe(w, 8 * b, 2), i1 = __builtin_amdgcn_ubfe(w, 8 * b + 2, 2);
                 float ds[4];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) ds[q] = acc[i][j][4 * b + q];
                 const float d0 = i0 == 0u ? ds[0] : i0 == 1u ? ds[1] : ds[2];
                 const float d1 = i1 == 1u ? ds[1] : i1 == 2u ? ds[2] : ds[3];
-                const float s0 = __builtin_bit_cast(float, sv << 16);
-                const float s1 = __builtin_bit_cast(float, sv & 0xFFFF0000u);
-                const uint32_t rr = bf16x2_rne(sqrt_for_bf16(s0), sqrt_for_bf16(s1));   // relu(h), exact
+                const uint32_t rr = bf16x2_rne(rt[b][0], rt[b][1]);   // relu(h), exact
                 const float r0 = __builtin_bit_cast(float, rr << 16);
                 const float r1 = __builtin_bit_cast(float, rr & 0xFFFF0000u);
-                *loc = bf16x2_rne(d0 * 2.0f * r0, d1 * 2.0f * r1);
+                *loc[b] = bf16x2_rne(d0 * 2.0f * r0, d1 * 2.0f * r1);
               }
             }
           }
