@@ -797,8 +797,8 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
               uint32_t v[2];
 #pragma unroll
               for (int e = 0; e < 2; ++e) {
-                // h rounded to bf16 (RNE), relu'd, squared (act_square) and rounded
-                const uint32_t r = relu_bits2(bf16x2_rne(acc[i][j][4 * b + 2 * e], acc[i][j][4 * b + 2 * e + 1]));
+                // h relu'd and rounded to bf16 (RNE), squared (act_square) and rounded
+                const uint32_t r = bf16x2_rne(relu_f32(acc[i][j][4 * b + 2 * e]), relu_f32(acc[i][j][4 * b + 2 * e + 1]));
                 if (g.act_square) {
                   const float lo = __builtin_bit_cast(float, r << 16), hi = __builtin_bit_cast(float, r & 0xFFFF0000u);
                   v[e] = bf16x2_rne(lo * lo, hi * hi);
@@ -809,23 +809,50 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
               mine[b] = make_uint2(v[0], v[1]);
             }
           } else {
+            float x[4][4];   // the stored activation of features 8b + 4h + 0..3
+            bool tiny = false;   // a subnormal stored s (the raw square root flushes it)
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
               const int64_t f = f32 + 8 * b + 4 * lhalf;
               uint2 a = make_uint2(0u, 0u);
               if (t < g.N && f < g.f_valid) a = *(const uint2*)(g.act + t * g.ld_act + f);
-              uint32_t v[2];
 #pragma unroll
               for (int e = 0; e < 2; ++e) {
                 const uint32_t w = e ? a.y : a.x;
-                float x0 = __builtin_bit_cast(float, w << 16), x1 = __builtin_bit_cast(float, w & 0xFFFF0000u);
-                if (g.act_square) {   // r = bf16(sqrt(a)) recovers relu(h) exactly
-                  const uint32_t rr = bf16x2_rne(sqrt_for_bf16(x0), sqrt_for_bf16(x1));
-                  x0 = __builtin_bit_cast(float, rr << 16);
-                  x1 = __builtin_bit_cast(float, rr & 0xFFFF0000u);
-                }
-                v[e] = bf16x2_rne(acc[i][j][4 * b + 2 * e] * 2.0f * x0, acc[i][j][4 * b + 2 * e + 1] * 2.0f * x1);
+                x[b][2 * e] = __builtin_bit_cast(float, w << 16);
+                x[b][2 * e + 1] = __builtin_bit_cast(float, w & 0xFFFF0000u);
+                tiny |= __builtin_amdgcn_classf(x[b][2 * e], 0x80) | __builtin_amdgcn_classf(x[b][2 * e + 1], 0x80);
               }
+            }
+            if (g.act_square) {   // r = bf16(sqrt(s)) recovers relu(h) exactly
+              float rt[4][4];
+              if (__builtin_amdgcn_ballot_w64(tiny) == 0) {
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+#pragma unroll
+                  for (int q = 0; q < 4; ++q) rt[b][q] = __builtin_amdgcn_sqrtf(x[b][q]);
+              } else {
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+#pragma unroll
+                  for (int q = 0; q < 4; ++q) rt[b][q] = sqrt_for_bf16(x[b][q]);
+              }
+#pragma unroll
+              for (int b = 0; b < 4; ++b)
+#pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                  const uint32_t rr = bf16x2_rne(rt[b][2 * e], rt[b][2 * e + 1]);
+                  x[b][2 * e] = __builtin_bit_cast(float, rr << 16);
+                  x[b][2 * e + 1] = __builtin_bit_cast(float, rr & 0xFFFF0000u);
+                }
+            }
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+              uint32_t v[2];
+#pragma unroll
+              for (int e = 0; e < 2; ++e)
+                v[e] = bf16x2_rne(acc[i][j][4 * b + 2 * e] * 2.0f * x[b][2 * e],
+                                  acc[i][j][4 * b + 2 * e + 1] * 2.0f * x[b][2 * e + 1]);
               mine[b] = make_uint2(v[0], v[1]);
             }
           }
