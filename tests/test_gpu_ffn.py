@@ -281,3 +281,37 @@ def test_ste_equals_masked_when_at_most_two_positives():
     a, s = run_gpu(bits, mode="sparse"), run_gpu(bits, mode="ste")
     for k in ("dx",) + GRADS:
         assert rel_fro(s[k], a[k]) < 1e-2, k
+
+
+
+@pytest.mark.parametrize("mode", ["sparse", "dense"])
+def test_subnormal_activations_recover_relu(mode):
+    """x scaled by c = 2^-64 (exact in bf16) scales h by c, so most stored
+    s = bf16(h^2) are subnormal.  The backward recovers relu(h) from s as the
+    correctly rounded bf16 square root, which for subnormal s needs the
+    pre-scaled root (the raw one flushes them).  Expected: c times the
+    oracle's backward at c = 1 with relu(h) replaced by that root / c at the
+    GPU's kept positions; a flushing root would lose most of dx."""
+    T, d, F, r = 300, 512, 1376, 128
+    bits = ffn_inputs(T, d, F, r, seed_base=33)
+    sparse = mode == "sparse"
+    a = offn.from_bits(bits)
+    f = offn.forward(a["x"], a["U_up"], a["V_up"], a["U_down"], a["V_down"], sparse=sparse)
+    c = 2.0 ** -64
+    scaled = dict(bits)
+    scaled["x"] = obf.from_f64(a["x"] * c)
+    assert np.array_equal(obf.to_f64(scaled["x"]), a["x"] * c)   # every scaled x is a normal bf16
+    gpu = run_gpu(scaled, mode=mode)
+    kept = gpu["S"][gpu["mask"]]
+    assert np.mean(kept[kept > 0] < 2.0 ** -126) > 0.5, "most stored s should be subnormal"
+    root = obf.to_f64(obf.from_f64(np.sqrt(gpu["S"])))   # relu(h) as the kernel recovers it
+
+    def expected_dx(relu_h):
+        fe = dict(f, H=relu_h / c, mask=gpu["mask"])
+        return c * offn.backward(a["dY"], a["x"], a["U_up"], a["V_up"], a["U_down"], a["V_down"], fe)["dx"]
+
+    want = expected_dx(root)
+    assert rel_fro(gpu["dx"], want) <= TOL
+    # the check can tell a flushing root apart (CPU-side counterfactual)
+    flushed = expected_dx(np.where(gpu["S"] < 2.0 ** -126, 0.0, root))
+    assert rel_fro(flushed, want) > 0.5
