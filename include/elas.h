@@ -45,6 +45,20 @@
  * a padded row is itself a valid 2:4 row whose extra entries are zero.
  * Per kept value this is 2 bytes plus 2 bits: 0.5625 of dense bf16, the ratio
  * of the paper's Table 2 (Sec. 4.2.2).
+ *
+ * Tiled compressed layout (the FFN's saved S)
+ * -------------------------------------------
+ * elas_lowrank_ffn_fwd stores the compressed S in the same buffers
+ * (M x ldv values, M x ldm bytes, M = T) with the same row contents, but
+ * tiled so that the 2:4 products read whole contiguous blocks: rows are cut
+ * into blocks of 256 (the last block holds the R = M - 256 b remaining rows,
+ * otherwise R = 256), and within a row block each row's entries into blocks
+ * of BW = 32 values (ldv) or BW = 8 metadata bytes (ldm), i.e. 64 features.
+ * Entry block c of row block b holds its R rows x BW entries row-major and
+ * contiguously; blocks follow one another by row block, then entry block.
+ * Entry j of row i (values: ld = ldv, BW = 32; metadata: ld = ldm, BW = 8) is
+ *   element  (i / 256) * 256 * ld + (j / BW) * R * BW + (i % 256) * BW + j % BW.
+ * elas_sparsify_24 and elas_spmm_24 use the row layout above.
  */
 #ifndef ELAS_H
 #define ELAS_H
@@ -145,10 +159,11 @@ int elas_spmm_24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, int64
  * Outputs (bf16, device, written):
  *   y      [T,d]
  *   P      [T,r]   saved for the backward (P = x U_up, rounded to bf16)
- *   s_vals sparse mode: [T x elas_vals_ld(d_ff)] compressed S (kept s in bf16)
- *          dense mode:  [T x d_ff] dense S = relu(H)^2 in bf16
- *   s_meta sparse mode: [T x elas_meta_ld(d_ff)] 2-bit indices; dense mode:
- *          not used (may be NULL)
+ *   s_vals sparse mode: T x elas_vals_ld(d_ff) values, compressed S (kept s in
+ *          bf16) in the tiled layout above
+ *          dense mode:  [T x d_ff] dense S = relu(H)^2 in bf16, row-major
+ *   s_meta sparse mode: T x elas_meta_ld(d_ff) bytes, its 2-bit indices, tiled;
+ *          dense mode: not used (may be NULL)
  *   Z      [T,r]   saved for the backward
  * Rounding points: P, H (before ReLU^2), the kept s, Z and y are rounded to
  * bf16 (nearest-even); every product accumulates in fp32.  The 2:4 selection

@@ -174,8 +174,10 @@ def elas_lowrank_ffn_fwd(x, U_up, V_up, U_down, V_down, flags: int = 0, out: dic
                          workspace: torch.Tensor | None = None) -> dict:
     """Forward of the low-rank 2:4 FFN.  Returns dict(y, P, s_vals, s_meta, Z).
 
-    With ``flags=ELAS_MODE_DENSE`` s_vals is the dense [T, d_ff] activation and
-    s_meta is None.  With ``ELAS_FACTORS_AB`` the factors are passed transposed
+    s_vals [T, elas_vals_ld(d_ff)] and s_meta [T, elas_meta_ld(d_ff)] hold the
+    compressed S in the tiled layout of include/elas.h (the tensors' shapes
+    give the sizes, not row positions).  With ``flags=ELAS_MODE_DENSE`` s_vals
+    is the dense row-major [T, d_ff] activation and s_meta is None.  With ``ELAS_FACTORS_AB`` the factors are passed transposed
     (U_up^T [r, d], V_up^T [d_ff, r], U_down^T [r, d_ff], V_down^T [d, r])."""
     T, d = x.shape
     ab = bool(flags & ELAS_FACTORS_AB)

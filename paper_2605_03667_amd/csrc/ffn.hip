@@ -483,6 +483,7 @@ hipError_t gemm_tt_f32(const char* tag, const uint16_t* A, int64_t lda, const ui
   g.A = A; g.lda = lda; g.Am = Am; g.ldam = ldam; g.B = B; g.ldb = ldb;
   g.M = M; g.N = N; g.K = K; g.m_valid = M; g.ka_valid = K; g.kb_valid = K;
   g.k_split = p.k_split; g.C = part; g.ldc = N;
+  if (AMODE == OP_TSP) g.tok = K;   // the compressed operand is tiled over its K (token) rows
   const dim3 rgrid((unsigned)cdiv(N, 64), (unsigned)cdiv(rows_out, 64));
   if (p.stream_steps > 0) {
     static_assert(Cfg::BM == 256 && Cfg::BN == 256, "stream-K partial tiles are 256 x 256");
@@ -633,11 +634,11 @@ hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
     GemmArgs g{};
     g.A = V_upT; g.lda = r; g.B = a.P; g.ldb = r;
     g.M = Fp; g.N = T; g.K = r; g.m_valid = F_rows; g.ka_valid = r; g.kb_valid = r;
-    g.sv = a.s_vals; g.sm = a.s_meta; g.ldv = vals_ld(F); g.ldm = meta_ld(F);
+    g.sv = a.s_vals; g.sm = a.s_meta; g.ldv = vals_ld(F); g.ldm = meta_ld(F); g.tok = T;   // S written tiled
     ELAS_TRY(launch_staged<EPI_SPARSIFY>("k2_up_relu2_sparsify", g, st));
     // Z = S U_down on the 2:4 operand
     GemmArgs z{};
-    z.A = a.s_vals; z.lda = vals_ld(F); z.Am = a.s_meta; z.ldam = meta_ld(F);
+    z.A = a.s_vals; z.lda = vals_ld(F); z.Am = a.s_meta; z.ldam = meta_ld(F); z.a_tiled = 1; z.tok = T;
     z.B = U_downT; z.ldb = ld_ud;
     z.M = T; z.N = r; z.K = Fp; z.m_valid = T; z.ka_valid = Fp; z.kb_valid = ld_ud;
     z.C = a.Z; z.ldc = r;
@@ -694,14 +695,14 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
     GemmArgs g{};
     g.A = a.U_down; g.lda = r; g.B = w.dZ; g.ldb = r;
     g.M = Fp; g.N = T; g.K = r; g.m_valid = F; g.ka_valid = r; g.kb_valid = r;
-    g.sv = a.s_vals; g.sm = a.s_meta; g.ldv = ldv; g.ldm = ldm; g.dv = w.dH;
+    g.sv = a.s_vals; g.sm = a.s_meta; g.ldv = ldv; g.ldm = ldm; g.dv = w.dH; g.tok = T;   // S read, dH written, tiled
     ELAS_TRY(launch_staged<EPI_DH>("b3_dH_masked", g, st));
     // dU_down = S^T dZ from the compressed S
     ELAS_TRY(gemm_tt_f32<OP_TSP>("b4_dU_down", a.s_vals, ldv, a.s_meta, ldm, w.dZ, r, Fp, r, T, w.part, a.dU_down, F,
                                  false, r, st));
     // dP = dH V_up^T on the 2:4 operand (V_up [r x F] is already K-contiguous)
     GemmArgs p{};
-    p.A = w.dH; p.lda = ldv; p.Am = a.s_meta; p.ldam = ldm;
+    p.A = w.dH; p.lda = ldv; p.Am = a.s_meta; p.ldam = ldm; p.a_tiled = 1; p.tok = T;
     p.B = a.V_up; p.ldb = F;
     p.M = T; p.N = r; p.K = Fp; p.m_valid = T; p.ka_valid = Fp; p.kb_valid = F;
     p.C = w.dP; p.ldc = r;

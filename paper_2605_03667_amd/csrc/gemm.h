@@ -76,10 +76,11 @@ struct GemmArgs {
   void* C;             // EPI_BF16: bf16 [M x N] pitch ldc; EPI_F32: float [splits][M][N]
   int64_t ldc;
   // EPI_SPARSIFY / EPI_DH: C rows are features f (M), columns are tokens t (N).
-  uint16_t* sv;        // kept values of S [N x ldv]: written (SPARSIFY) / read (DH)
-  uint8_t* sm;         // metadata of S [N x ldm]
+  // The compressed tensors are tiled (tiled_index) with tok = N rows.
+  uint16_t* sv;        // kept values of S (N rows, pitch ldv): written (SPARSIFY) / read (DH)
+  uint8_t* sm;         // metadata of S (N rows, pitch ldm)
   int64_t ldv, ldm;
-  uint16_t* dv;        // EPI_DH: kept values of dH [N x ldv], written
+  uint16_t* dv;        // EPI_DH: kept values of dH (N rows, pitch ldv), written
   // EPI_ACT_DENSE / EPI_DH_DENSE: dense [N x ld_act] activations (tokens as
   // rows), features f < f_valid only.
   uint16_t* act;       // ACT_DENSE: written; DH_DENSE: read (r = bf16(sqrt(a)) if act_square, else a)
@@ -98,7 +99,33 @@ struct GemmArgs {
   // its range touches to C + (w * stream_segs + j) * BM * BN (row-major).
   int64_t stream_steps;
   int stream_segs;
+  // Compressed 2:4 tensors in the tiled layout (tiled_index below): the 2:4
+  // operand of OP_SP when a_tiled is set (OP_TSP and the staged epilogues
+  // always), with tok token rows.
+  int a_tiled;
+  int64_t tok;
 };
+
+// Tiled layout of a compressed 2:4 tensor with tok rows (tokens) and row pitch
+// ld (values, or metadata bytes): rows in blocks of 256 (the last block holds
+// the R < 256 remaining rows) and each row's entries in blocks of BW (32
+// values or 8 metadata bytes: 64 features); block (row block, entry block)
+// holds its R rows x BW entries row-major and contiguously, blocks ordered by
+// row block, then entry block.  Index of entry j of row t:
+template <int BW>
+__device__ __forceinline__ int64_t tiled_index(int64_t t, int64_t j, int64_t tok, int64_t ld) {
+  const int64_t tb = t >> 8;
+  const int64_t R = tok - (tb << 8) < 256 ? tok - (tb << 8) : 256;
+  return (tb << 8) * ld + (j / BW) * R * BW + (t & 255) * BW + (j % BW);
+}
+// Start of the step at dense contraction index k0 (a multiple of 64) for rows
+// from row0 (inside one row block): entry block k0/64, row row0 % 256.
+template <int BW>
+__device__ __forceinline__ int64_t tiled_step(int64_t row0, int64_t k0, int64_t tok, int64_t ld) {
+  const int64_t tb = row0 >> 8;
+  const int64_t R = tok - (tb << 8) < 256 ? tok - (tb << 8) : 256;
+  return (tb << 8) * ld + (k0 >> 6) * R * BW + (row0 & 255) * BW;
+}
 
 template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int AMODE_, int BMODE_, int EPI_, bool M_FAST_,
           int STAGES_ = 2, bool PIPE_ = true, bool PIN_ = false, int SPK_ = 128, int DEEP_ = 0>
@@ -157,6 +184,7 @@ struct GemmCfg {
   // uniform two-stage ring only): the metadata rows go in as dword DMAs of 256
   // bytes, META_DMA_PER_WAVE per wave, so their area is rounded up to that.
   static constexpr bool PRE_S = EPI_ == EPI_DH && DEEP_ == 0 && STAGES_ == 2;
+  static_assert(EPI_ != EPI_DH || PRE_S, "EPI_DH copies its S tile during the last K step");
   static constexpr int META_DMA_PER_WAVE = (BN_ * META_PITCH / 4 + 64 * NW - 1) / (64 * NW);
   static constexpr int META_BYTES = PRE_S ? META_DMA_PER_WAVE * NW * 256 : (BN_ * META_PITCH + 15) / 16 * 16;
   static constexpr int A_PART = A_BYTES + AM_BYTES;   // one stage of A (and its metadata)
@@ -290,10 +318,11 @@ struct DmaTile {
   static constexpr int KPC = KEPT ? 16 : 8;    // dense K per 16-byte chunk
   // Issue this wave's loads j in [J0, J1) for the step at k0 into the LDS
   // buffer at byte address lds (wave-uniform).
+  // tok > 0 (kept values only): the tiled layout with tok rows.
   template <int J0, int J1>
   __device__ __forceinline__ static void issue(const uint16_t* __restrict__ p, int64_t ld, int64_t row0,
                                                int64_t rows_valid, int64_t k0, int64_t k_valid, uint32_t lds,
-                                               int wave, int lane) {
+                                               int wave, int lane, int64_t tok = 0) {
 #pragma unroll
     for (int j = J0; j < J1; ++j) {
       const int blk = wave * PER_WAVE + j;
@@ -301,8 +330,11 @@ struct DmaTile {
       const int row = off / ROWB, pos = (off % ROWB) / 16;
       const int c = swz_row<ROWB>(row, pos);   // the swizzle is an involution in the chunk index
       const int64_t grow = row0 + row, gk = k0 + (int64_t)c * KPC;
-      const void* src = (grow < rows_valid && gk < k_valid) ? (const void*)(p + grow * ld + (KEPT ? gk / 2 : gk))
-                                                           : (const void*)g_dma_zero;
+      int64_t idx = grow * ld + (KEPT ? gk / 2 : gk);
+      if constexpr (KEPT) {
+        if (tok > 0) idx = tiled_index<32>(grow, gk / 2, tok, ld);
+      }
+      const void* src = (grow < rows_valid && gk < k_valid) ? (const void*)(p + idx) : (const void*)g_dma_zero;
       dma_b128(src, __builtin_amdgcn_readfirstlane(lds + blk * 1024));
     }
   }
@@ -333,19 +365,20 @@ struct DmaMeta {
   static constexpr int BLOCKS = ROWS * MROWB / 256;
   static constexpr int PER_WAVE = BLOCKS / NW;
   static_assert(BLOCKS % NW == 0, "meta blocks per wave");
+  // tok > 0: the tiled layout with tok rows.
   template <int J0, int J1>
   __device__ __forceinline__ static void issue(const uint8_t* __restrict__ pm, int64_t ldm, int64_t row0,
                                                int64_t rows_valid, int64_t k0, int64_t k_valid, uint32_t lds,
-                                               int wave, int lane) {
+                                               int wave, int lane, int64_t tok = 0) {
 #pragma unroll
     for (int j = J0; j < J1; ++j) {
       const int blk = wave * PER_WAVE + j;
       const int off = blk * 256 + lane * 4;
       const int row = off / MROWB, dw = (off % MROWB) / 4;   // dword dw covers dense K 32 dw .. 32 dw + 31
       const int64_t grow = row0 + row;
-      const void* src = (grow < rows_valid && k0 + 32 * (dw + 1) <= k_valid)
-                            ? (const void*)(pm + grow * ldm + k0 / 8 + dw * 4)
-                            : (const void*)g_dma_zero;
+      const int64_t idx = tok > 0 ? tiled_index<8>(grow, k0 / 8 + dw * 4, tok, ldm) : grow * ldm + k0 / 8 + dw * 4;
+      const void* src = (grow < rows_valid && k0 + 32 * (dw + 1) <= k_valid) ? (const void*)(pm + idx)
+                                                                             : (const void*)g_dma_zero;
       dma_b32(src, __builtin_amdgcn_readfirstlane(lds + blk * 256));
     }
   }
@@ -454,33 +487,49 @@ struct StagerKMSP {
   static constexpr int CHUNKS = ROWS / 16;
   static constexpr int NU = 64 * CHUNKS / NT;
   static_assert((64 * CHUNKS) % NT == 0, "units per thread");
+  // Unit q (16 features of one contraction row): chunk q % 4 of entry block
+  // q / 256 (64 features) at row (q / 4) % 64, so that the 64 lanes of a wave
+  // read 16 rows x 64 bytes of one entry block, 1 KB contiguous in the tiled
+  // layout.
+  __device__ __forceinline__ static int unit_k(int q) { return (q >> 2) & 63; }
+  __device__ __forceinline__ static int unit_c(int q) { return (q >> 8) * 4 + (q & 3); }
   uint4 v[NU];
   uint16_t m[NU];
+  // The compressed tensor is in the tiled layout with tok rows (tokens =
+  // contraction rows here).
+  // The step's rows k0 .. k0+63 lie in one block of 256 rows (R of them
+  // exist), so every piece is a 32-bit offset from the step's block start.
   __device__ __forceinline__ void load(const uint16_t* __restrict__ pv, int64_t ldv, const uint8_t* __restrict__ pm,
                                        int64_t ldm, int64_t col0, int64_t cols_valid, int64_t k0, int64_t k_valid,
-                                       int tid) {
+                                       int tid, int64_t tok) {
+    const int64_t tb0 = k0 & ~(int64_t)255;
+    const int R = (int)(tok - tb0 < 256 ? tok - tb0 : 256);
+    const uint16_t* vb = pv + tiled_step<32>(k0, col0, tok, ldv);
+    const uint8_t* mb = pm + tiled_step<8>(k0, col0, tok, ldm);
 #pragma unroll
     for (int u = 0; u < NU; ++u) {
-      const int q = u * NT + tid, k = q / CHUNKS, c = q % CHUNKS;
+      const int q = u * NT + tid, k = unit_k(q), c = unit_c(q);
       const int64_t gk = k0 + k, f = col0 + 16 * c;
       v[u] = make_uint4(0u, 0u, 0u, 0u);
       m[u] = 0u;
       if (gk < k_valid && f < cols_valid) {
-        v[u] = *(const uint4*)(pv + gk * ldv + f / 2);
-        m[u] = *(const uint16_t*)(pm + gk * ldm + f / 8);
+        v[u] = *(const uint4*)(vb + ((c >> 2) * R * 32 + k * 32 + (c & 3) * 8));
+        m[u] = *(const uint16_t*)(mb + ((c >> 2) * R * 8 + k * 8 + (c & 3) * 2));
       }
     }
   }
-  // Unchecked path (tile and step inside the matrix): per-lane byte offsets
-  // from the step's first row and the tile's first column, constant over the
-  // steps, and a wave-uniform base per step.
-  __device__ __forceinline__ static void lane_offs(int64_t ldv, int64_t ldm, int tid, uint32_t (&ov)[NU],
-                                                   uint32_t (&om)[NU]) {
+  // Unchecked path (tile and step inside the matrix, step inside a full block
+  // of 256 rows): per-lane byte offsets from the step's block start
+  // (tiled_step of its first row and the tile's first column), constant over
+  // the steps, and a wave-uniform base per step.  Thread unit (k, c) reads
+  // entry block c / 4 at row k, entries 8 (c % 4) .. (values) and 2 (c % 4) ..
+  // (metadata bytes).
+  __device__ __forceinline__ static void lane_offs(int tid, uint32_t (&ov)[NU], uint32_t (&om)[NU]) {
 #pragma unroll
     for (int u = 0; u < NU; ++u) {
-      const int q = u * NT + tid, k = q / CHUNKS, c = q % CHUNKS;
-      ov[u] = (uint32_t)k * (uint32_t)(ldv * 2) + (uint32_t)c * 16u;
-      om[u] = (uint32_t)k * (uint32_t)ldm + (uint32_t)c * 2u;
+      const int q = u * NT + tid, k = unit_k(q), c = unit_c(q);
+      ov[u] = (uint32_t)((c >> 2) * 256 * 32 + k * 32 + (c & 3) * 8) * 2u;
+      om[u] = (uint32_t)((c >> 2) * 256 * 8 + k * 8 + (c & 3) * 2);
     }
   }
   __device__ __forceinline__ void load_fast(const char* vbase, const char* mbase, const uint32_t (&ov)[NU],
@@ -497,7 +546,7 @@ struct StagerKMSP {
   __device__ __forceinline__ void store(char* lds, int tid) const {
 #pragma unroll
     for (int u = 0; u < NU; ++u) {
-      const int q = u * NT + tid, k = q / CHUNKS, c = q % CHUNKS;
+      const int q = u * NT + tid, k = unit_k(q), c = unit_c(q);
       char* dst = lds + k * ROWB + (km_swz(k, c) << 5);
       *(uint4*)dst = expand2(make_uint2(v[u].x, v[u].y), m[u] & 0xFFu);
       *(uint4*)(dst + 16) = expand2(make_uint2(v[u].z, v[u].w), m[u] >> 8);
@@ -905,29 +954,6 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       if constexpr (Cfg::PRE_S) {
         pre();            // the S tile is in LDS (copied during the last K step)
         __syncthreads();
-      } else if constexpr (Cfg::EPI == EPI_DH) {
-        // stored S rows of this tile -> LDS
-        constexpr int VCH = BN * (BM / 16);               // 16-byte value chunks
-#pragma unroll
-        for (int it = 0; it < VCH / NT; ++it) {
-          const int q = it * NT + tid, row = q / (BM / 16), c = q % (BM / 16);
-          if (row < t_end && c * 16 < f_end) {
-            const uint4 v = *(const uint4*)(g.sv + (n0 + row) * g.ldv + m0 / 2 + c * 8);
-            uint32_t* d = (uint32_t*)(lv + row * BM + (c ^ (row & 15)) * 16);
-            d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
-          }
-        }
-        constexpr int MCH = BN * (BM / 64);               // 8-byte metadata chunks
-#pragma unroll
-        for (int it = 0; it < (MCH + NT - 1) / NT; ++it) {
-          const int q = it * NT + tid, row = q / (BM / 64), c = q % (BM / 64);
-          if (q < MCH && row < t_end && c * 64 < f_end) {
-            const uint2 v = *(const uint2*)(g.sm + (n0 + row) * g.ldm + m0 / 8 + c * 8);
-            uint32_t* d = (uint32_t*)(lm + row * MP + c * 8);
-            d[0] = v.x; d[1] = v.y;
-          }
-        }
-        __syncthreads();
       }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
@@ -1008,29 +1034,37 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         }
       __syncthreads();
 
-      // LDS -> global: whole 16-byte pieces of each token row
-      uint16_t* dst = Cfg::EPI == EPI_SPARSIFY ? g.sv : g.dv;
+      // LDS -> global in the tiled layout: the tile's tokens lie in one block
+      // of 256 rows (R of them exist) and its features in BM/64 entry blocks,
+      // each written as one contiguous run (64 bytes of values, 8 of metadata
+      // per token).  Thread q takes 16-byte piece q % 4 of token (q / 4) % BN
+      // in entry block q / (4 BN).
+      uint16_t* dst = (Cfg::EPI == EPI_SPARSIFY ? g.sv : g.dv) + tiled_step<32>(n0, m0, g.tok, g.ldv);
+      const int64_t Rb = g.tok - (n0 & ~(int64_t)255) < 256 ? g.tok - (n0 & ~(int64_t)255) : 256;
+      int td = tid;   // laundered: offsets formed here, not kept live across the main loop
+      asm volatile("" : "+v"(td));
       constexpr int VCH = BN * (BM / 16);
 #pragma unroll
       for (int it = 0; it < VCH / NT; ++it) {
-        const int q = it * NT + tid, row = q / (BM / 16), c = q % (BM / 16);
+        const int q = it * NT + td, kbi = q / (4 * BN), row = (q / 4) % BN, c = kbi * 4 + q % 4;
         if (row < t_end && c * 16 < f_end) {
           const uint32_t* sp = (const uint32_t*)(lv + row * BM + (c ^ (row & 15)) * 16);
           // non-temporal: the compressed rows stream out and should not evict
           // the weight panel this XCD keeps in L2
           const u32x4 v = {sp[0], sp[1], sp[2], sp[3]};
-          __builtin_nontemporal_store(v, (u32x4*)(dst + (n0 + row) * g.ldv + m0 / 2 + c * 8));
+          __builtin_nontemporal_store(v, (u32x4*)(dst + kbi * Rb * 32 + row * 32 + (q % 4) * 8));
         }
       }
       if constexpr (Cfg::EPI == EPI_SPARSIFY) {
+        uint8_t* mdst = g.sm + tiled_step<8>(n0, m0, g.tok, g.ldm);
         constexpr int MCH = BN * (BM / 64);
 #pragma unroll
         for (int it = 0; it < (MCH + NT - 1) / NT; ++it) {
-          const int q = it * NT + tid, row = q / (BM / 64), c = q % (BM / 64);
-          if (q < MCH && row < t_end && c * 64 < f_end) {
-            const uint32_t* sp = (const uint32_t*)(lm + row * MP + c * 8);
+          const int q = it * NT + td, kbi = q / BN, row = q % BN;
+          if (q < MCH && row < t_end && kbi * 64 < f_end) {
+            const uint32_t* sp = (const uint32_t*)(lm + row * MP + kbi * 8);
             const u32x2 v = {sp[0], sp[1]};
-            __builtin_nontemporal_store(v, (u32x2*)(g.sm + (n0 + row) * g.ldm + m0 / 8 + c * 8));
+            __builtin_nontemporal_store(v, (u32x2*)(mdst + kbi * Rb * 8 + row * 8));
           }
         }
       }
@@ -1048,12 +1082,12 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     // the same for every tile.
     uint32_t offA[LA], offB[LB], offM[LM > 0 ? LM : 1];
 #pragma unroll
-    for (int j = 0; j < LA; ++j) offA[j] = TA::lane_off(j, g.lda, wave, lane);
+    for (int j = 0; j < LA; ++j) offA[j] = TA::lane_off(j, (SPARSE && g.a_tiled) ? 32 : g.lda, wave, lane);
 #pragma unroll
     for (int j = 0; j < LB; ++j) offB[j] = TB::lane_off(j, g.ldb, wave, lane);
     if constexpr (SPARSE) {
 #pragma unroll
-      for (int j = 0; j < LM; ++j) offM[j] = TMeta::lane_off(j, g.ldam, wave, lane);
+      for (int j = 0; j < LM; ++j) offM[j] = TMeta::lane_off(j, g.a_tiled ? 8 : g.ldam, wave, lane);
     }
     // Steps [0, steps_in) of a tile inside both operands read no element
     // outside them: their loads skip the bounds checks.
@@ -1074,16 +1108,27 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       const int64_t k0 = kbeg + (int64_t)step * BK;
       const uint32_t base = smem_lds + a_off;
       if (step < s_in) {
-        TA::template issue_fast<0, LA>(TA::step_base(g.A, g.lda, m0, k0), offA, base, wave);
-        if constexpr (SPARSE)
-          TMeta::template issue_fast<0, LM>(TMeta::step_base(g.Am, g.ldam, m0, k0), offM, base + Cfg::A_BYTES, wave);
+        if (SPARSE && g.a_tiled) {
+          // tiled 2:4 operand: the step is one contiguous block of rows x 32 values (8 bytes)
+          TA::template issue_fast<0, LA>((const char*)(g.A + tiled_step<32>(m0, k0, g.tok, g.lda)), offA, base, wave);
+          TMeta::template issue_fast<0, LM>((const char*)(g.Am + tiled_step<8>(m0, k0, g.tok, g.ldam)), offM,
+                                            base + Cfg::A_BYTES, wave);
+        } else {
+          TA::template issue_fast<0, LA>(TA::step_base(g.A, g.lda, m0, k0), offA, base, wave);
+          if constexpr (SPARSE)
+            TMeta::template issue_fast<0, LM>(TMeta::step_base(g.Am, g.ldam, m0, k0), offM, base + Cfg::A_BYTES, wave);
+        }
       } else {
         int64_t kc = uniform_i64(k0);
         int lc = lane;
         asm volatile("" : "+s"(kc), "+v"(lc));
-        TA::template issue<0, LA>(g.A, g.lda, m0, g.m_valid, kc, g.ka_valid, base, wave, lc);
-        if constexpr (SPARSE)
-          TMeta::template issue<0, LM>(g.Am, g.ldam, m0, g.m_valid, kc, g.ka_valid, base + Cfg::A_BYTES, wave, lc);
+        if constexpr (SPARSE) {
+          const int64_t tk = g.a_tiled ? g.tok : 0;
+          TA::template issue<0, LA>(g.A, g.lda, m0, g.m_valid, kc, g.ka_valid, base, wave, lc, tk);
+          TMeta::template issue<0, LM>(g.Am, g.ldam, m0, g.m_valid, kc, g.ka_valid, base + Cfg::A_BYTES, wave, lc, tk);
+        } else {
+          TA::template issue<0, LA>(g.A, g.lda, m0, g.m_valid, kc, g.ka_valid, base, wave, lc);
+        }
       }
     };
     auto issue_b = [&](int64_t n0, int s_in, int step, uint32_t b_off) __attribute__((always_inline)) {
@@ -1200,49 +1245,40 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           constexpr int MPD = Cfg::META_PITCH / 4;    // dwords per metadata row (the last is pad)
           constexpr int MPW = Cfg::META_DMA_PER_WAVE;
           const uint32_t lm_off = STAGES * Cfg::STAGE;
-          if (__builtin_amdgcn_readfirstlane((int)(t_end >= BN && f_end >= BM))) {
-            // whole tile inside: wave-uniform bases, 32-bit lane offsets; pad
-            // and surplus metadata lanes re-read their row's first dword
-            const char* vbase = (const char*)(g.sv + tn0 * g.ldv + tm0 / 2);
-            const char* mbase = (const char*)(g.sm + tn0 * g.ldm + tm0 / 8);
+          // The stored S is tiled and the tile's tokens lie in one block of
+          // 256 rows (R of them exist): value chunk c of token row t is
+          // entries 8 (c % 4) .. of entry block c / 4, metadata dword w is
+          // bytes 4 (w % 2) .. of entry block w / 2, at 32-bit offsets from
+          // wave-uniform bases.  Pieces outside the matrix (rows >= t_end,
+          // features >= f_end, a row's pad dword) re-read a valid piece of
+          // the tile instead: the epilogue never reads those LDS positions.
+          const int64_t Rb = g.tok - (tn0 & ~(int64_t)255) < 256 ? g.tok - (tn0 & ~(int64_t)255) : 256;
+          const char* vbase = (const char*)(g.sv + tiled_step<32>(tn0, tm0, g.tok, g.ldv));
+          const char* mbase = (const char*)(g.sm + tiled_step<8>(tn0, tm0, g.tok, g.ldm));
+          const int t_last = (int)(t_end < BN ? t_end : BN) - 1;
+          const int c_lim = (int)(f_end < BM ? f_end : BM) / 16;     // valid value chunks per row
+          // lane index laundered so that the offsets are formed here rather
+          // than hoisted out of the main loop into live registers
+          int ln = lane;
+          asm volatile("" : "+v"(ln));
 #pragma unroll
-            for (int j = 0; j < VPW; ++j) {
-              const int blk = wave * VPW + j;
-              const int b = blk * 1024 + lane * 16;
-              const int row = b / BM, c = ((b % BM) / 16) ^ (row & 15);
-              dma_b128_nt_s(vbase, (uint32_t)row * (uint32_t)(g.ldv * 2) + (uint32_t)c * 16u, smem_lds + off + blk * 1024);
-            }
+          for (int j = 0; j < VPW; ++j) {
+            const int blk = wave * VPW + j;
+            const int b = blk * 1024 + ln * 16;
+            int row = b / BM, c = ((b % BM) / 16) ^ (row & 15);
+            row = row < t_last ? row : t_last;
+            c = c < c_lim ? c : 0;
+            const uint32_t o = (uint32_t)((c >> 2) * (int)Rb * 32 + row * 32 + (c & 3) * 8) * 2u;
+            dma_b128_nt_s(vbase, o, smem_lds + off + blk * 1024);
+          }
 #pragma unroll
-            for (int j = 0; j < MPW; ++j) {
-              const int blk = wave * MPW + j;
-              const int q = blk * 64 + lane, row = q / MPD, w = q % MPD;
-              const bool real = row < BN && w < MPD - 1;
-              dma_b32_nt_s(mbase, real ? (uint32_t)row * (uint32_t)g.ldm + 4u * (uint32_t)w : 0u,
-                           smem_lds + lm_off + blk * 256);
-            }
-          } else {
-            // edge tile: checked addresses (lane index laundered so that they
-            // are formed here rather than kept live across the main loop)
-            int lc = lane;
-            asm volatile("" : "+v"(lc));
-#pragma unroll
-            for (int j = 0; j < VPW; ++j) {
-              const int blk = wave * VPW + j;
-              const int b = blk * 1024 + lc * 16;
-              const int row = b / BM, c = ((b % BM) / 16) ^ (row & 15);
-              const void* src = (row < t_end && c * 16 < f_end) ? (const void*)(g.sv + (tn0 + row) * g.ldv + tm0 / 2 + c * 8)
-                                                                : (const void*)g_dma_zero;
-              dma_b128_nt(src, __builtin_amdgcn_readfirstlane(smem_lds + off + blk * 1024));
-            }
-#pragma unroll
-            for (int j = 0; j < MPW; ++j) {
-              const int blk = wave * MPW + j;
-              const int q = blk * 64 + lc, row = q / MPD, w = q % MPD;
-              const void* src = (row < BN && row < t_end && w < MPD - 1 && 32 * w < f_end)
-                                    ? (const void*)(g.sm + (tn0 + row) * g.ldm + tm0 / 8 + 4 * w)
-                                    : (const void*)g_dma_zero;
-              dma_b32_nt(src, __builtin_amdgcn_readfirstlane(smem_lds + lm_off + blk * 256));
-            }
+          for (int j = 0; j < MPW; ++j) {
+            const int blk = wave * MPW + j;
+            const int q = blk * 64 + ln;
+            int row = q / MPD, w = q % MPD;
+            row = row < t_last ? row : t_last;
+            w = (w < MPD - 1 && 32 * w < f_end) ? w : 0;
+            dma_b32_nt_s(mbase, (uint32_t)((w >> 1) * (int)Rb * 8 + row * 8 + (w & 1) * 4), smem_lds + lm_off + blk * 256);
           }
         }
       };
@@ -1320,8 +1356,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     uint32_t offB[TB::PER_WAVE];
 #pragma unroll
     for (int j = 0; j < TB::PER_WAVE; ++j) offB[j] = TB::lane_off(j, g.ldb, wave, lane);
-    uint32_t aov[StagerKMSP<BM, NT>::NU], aom[StagerKMSP<BM, NT>::NU];
-    StagerKMSP<BM, NT>::lane_offs(g.lda, g.ldam, tid, aov, aom);
+
     // Accumulate steps [0, ns) of the K range starting at kb of the tile at (m0, n0).
     auto run_tile = [&](int64_t m0, int64_t n0, int64_t kb, int ns) __attribute__((always_inline)) {
       zero_acc();
@@ -1332,21 +1367,29 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         b_steps_in = k_in <= 0 ? 0 : (int)(k_in / BK < ns ? k_in / BK : ns);
       }
       b_steps_in = __builtin_amdgcn_readfirstlane(b_steps_in);
-      int a_steps_in = 0;   // steps whose A loads need no bounds checks
+      int a_steps_in = 0;   // steps whose A loads need no bounds checks (and lie in full row blocks)
       if (m0 + BM <= g.m_valid) {
-        const int64_t k_in = g.ka_valid - kb;
+        const int64_t k_full = g.ka_valid < (g.tok & ~(int64_t)255) ? g.ka_valid : (g.tok & ~(int64_t)255);
+        const int64_t k_in = k_full - kb;
         a_steps_in = k_in <= 0 ? 0 : (int)(k_in / BK < ns ? k_in / BK : ns);
       }
       a_steps_in = __builtin_amdgcn_readfirstlane(a_steps_in);
       auto load_a = [&](int step) __attribute__((always_inline)) {
         const int64_t k0 = kb + (int64_t)step * BK;
         if (step < a_steps_in) {
-          sa.load_fast((const char*)(g.A + k0 * g.lda) + m0, (const char*)(g.Am + k0 * g.ldam + m0 / 8), aov, aom);
+          // per-lane offsets formed here from a laundered thread index (cheaper
+          // than keeping them in registers across the main loop)
+          uint32_t aov[StagerKMSP<BM, NT>::NU], aom[StagerKMSP<BM, NT>::NU];
+          int tc = tid;
+          asm volatile("" : "+v"(tc));
+          StagerKMSP<BM, NT>::lane_offs(tc, aov, aom);
+          sa.load_fast((const char*)(g.A + tiled_step<32>(k0, m0, g.tok, g.lda)),
+                       (const char*)(g.Am + tiled_step<8>(k0, m0, g.tok, g.ldam)), aov, aom);
         } else {
           int64_t kc = uniform_i64(k0);   // addresses formed afresh (see the direct path)
           int tc = tid;
           asm volatile("" : "+s"(kc), "+v"(tc));
-          sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, kc, g.ka_valid, tc);
+          sa.load(g.A, g.lda, g.Am, g.ldam, m0, g.m_valid, kc, g.ka_valid, tc, g.tok);
         }
       };
       auto issue_b = [&](int step) __attribute__((always_inline)) {

@@ -1,6 +1,6 @@
-"""Shared test utilities: bf16 bit arrays <-> torch tensors, the padded
-compressed layout, and the comparison protocol between the GPU path and the
-oracle.  Holds none of the method's arithmetic."""
+"""Shared test utilities: bf16 bit arrays <-> torch tensors, the padded and
+tiled compressed layouts, and the comparison protocol between the GPU path
+and the oracle.  Holds none of the method's arithmetic."""
 from __future__ import annotations
 
 import numpy as np
@@ -34,6 +34,36 @@ def pad_compressed(vals: np.ndarray, meta: np.ndarray, N: int):
     m = np.full((M, meta_ld(N)), 0x44, dtype=np.uint8)
     m[:, : N // 8] = meta
     return v, m
+
+
+def untile(a, T: int, ld: int, bw: int):
+    """Row-major [T, ld] copy of a compressed tensor in the tiled layout the
+    FFN uses for its saved S (include/elas.h): rows in blocks of 256 (the last
+    block holds the R remaining rows), each block cut into entry blocks of bw
+    (32 values or 8 metadata bytes) that hold R rows x bw entries row-major,
+    one after the other.  Works on numpy arrays and torch tensors (on their
+    device); only the first T * ld entries are read."""
+    is_torch = isinstance(a, torch.Tensor)
+    flat = a.reshape(-1)[: T * ld]
+    parts = []
+    for t0 in range(0, T, 256):
+        R = min(256, T - t0)
+        blk = flat[t0 * ld: t0 * ld + R * ld].reshape(ld // bw, R, bw)
+        blk = blk.permute(1, 0, 2) if is_torch else blk.transpose(1, 0, 2)
+        parts.append(blk.reshape(R, ld))
+    if not parts:
+        return a.reshape(0, ld)
+    return torch.cat(parts) if is_torch else np.concatenate(parts)
+
+
+def tile(a: np.ndarray, bw: int) -> np.ndarray:
+    """Inverse of untile for a row-major [T, ld] numpy array (flat result)."""
+    T, ld = a.shape
+    parts = []
+    for t0 in range(0, T, 256):
+        R = min(256, T - t0)
+        parts.append(a[t0: t0 + R].reshape(R, ld // bw, bw).transpose(1, 0, 2).reshape(-1))
+    return np.concatenate(parts) if parts else a.reshape(-1)
 
 
 def check_padding(vals: np.ndarray, meta: np.ndarray, N: int):

@@ -6,6 +6,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 import paper_2605_03667_amd as elas
@@ -154,3 +155,26 @@ def test_fullrank_validation():
     assert call(x=None) == 1
     assert call(y=MIS) == 3
     assert call(T=0, x=None, y=None) == 0     # no tokens: nothing inspected
+
+
+def test_tiled_layout_helpers():
+    """The test-side conversion between row-major and the tiled layout of the
+    saved S matches the index formula the header states: entry j of row t at
+    (t // 256) * 256 * ld + (j // bw) * R * bw + (t % 256) * bw + j % bw, with
+    R the rows of t's block of 256 (ragged last block included)."""
+    from tests.helpers import tile, untile
+
+    def index(t, j, T, ld, bw):
+        tb = t // 256
+        R = min(256, T - 256 * tb)
+        return 256 * tb * ld + (j // bw) * R * bw + (t % 256) * bw + j % bw
+
+    for T in (1, 7, 256, 300, 513):
+        for ld, bw in ((64, 32), (96, 32), (16, 8), (24, 8)):
+            a = np.arange(T * ld).reshape(T, ld)
+            flat = np.empty(T * ld, dtype=a.dtype)
+            for t in range(T):
+                for j in range(ld):
+                    flat[index(t, j, T, ld, bw)] = a[t, j]
+            assert np.array_equal(tile(a, bw), flat)
+            assert np.array_equal(untile(flat.reshape(T, ld), T, ld, bw), a)

@@ -24,7 +24,7 @@ from oracle import bf16 as obf
 from oracle import ffn as offn
 from oracle import sparsify as osp
 from synthetic import CONFIGS, config_inputs, ffn_inputs, uniform_int_bf16
-from tests.helpers import check_padding, dev_bf16, host_bits, mask_gate, rel_fro
+from tests.helpers import check_padding, dev_bf16, host_bits, mask_gate, rel_fro, untile
 
 pytestmark = pytest.mark.gpu
 
@@ -51,10 +51,13 @@ def run_gpu(bits, rows=None, mode="sparse"):
     def rows_of(x):
         return x if idx is None else x.index_select(0, idx)
 
+    T = bits["x"].shape[0]
+    # the compressed S is tiled (include/elas.h); the dense one is row-major
+    sv = fwd["s_vals"] if mode == "dense" else untile(fwd["s_vals"], T, fwd["s_vals"].shape[1], 32)
     out = {
         "Y": obf.to_f64(host_bits(rows_of(fwd["y"]))), "P": obf.to_f64(host_bits(rows_of(fwd["P"]))),
         "Z": obf.to_f64(host_bits(rows_of(fwd["Z"]))), "dx": obf.to_f64(host_bits(rows_of(bwd["dx"]))),
-        "s_vals": host_bits(rows_of(fwd["s_vals"])),
+        "s_vals": host_bits(rows_of(sv)),
     }
     for k in GRADS:
         out[k] = bwd[k].cpu().numpy().astype(np.float64)
@@ -62,7 +65,7 @@ def run_gpu(bits, rows=None, mode="sparse"):
         out["S"] = obf.to_f64(out["s_vals"])
         out["mask"] = np.ones(out["S"].shape, dtype=bool)
     else:
-        out["s_meta"] = rows_of(fwd["s_meta"]).cpu().numpy()
+        out["s_meta"] = rows_of(untile(fwd["s_meta"], T, fwd["s_meta"].shape[1], 8)).cpu().numpy()
         check_padding(out["s_vals"], out["s_meta"], F)
         dense, mask = osp.decompress(out["s_vals"][:, : F // 2], out["s_meta"][:, : F // 8], F)
         out["mask"] = mask
