@@ -1041,8 +1041,11 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       // in entry block q / (4 BN).
       uint16_t* dst = (Cfg::EPI == EPI_SPARSIFY ? g.sv : g.dv) + tiled_step<32>(n0, m0, g.tok, g.ldv);
       const int64_t Rb = g.tok - (n0 & ~(int64_t)255) < 256 ? g.tok - (n0 & ~(int64_t)255) : 256;
-      int td = tid;   // laundered: offsets formed here, not kept live across the main loop
-      asm volatile("" : "+v"(td));
+      // k2: thread index laundered, so that these offsets are formed here and
+      // not kept live across the main loop (measured faster); b3 keeps them
+      // (measured faster there, within its registers)
+      int td = tid;
+      if constexpr (Cfg::EPI == EPI_SPARSIFY) asm volatile("" : "+v"(td));
       constexpr int VCH = BN * (BM / 16);
 #pragma unroll
       for (int it = 0; it < VCH / NT; ++it) {
