@@ -593,7 +593,17 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform, so derived LDS bases are scalar
   const int wm = wave / Cfg::WAVES_N, wn = wave % Cfg::WAVES_N;
   const int ntiles = g.tiles_m * g.tiles_n;
-  const int64_t kbeg = (int64_t)blockIdx.y * g.k_split;
+  // Split-K grids (gridDim.y contraction splits, a multiple of 8): workgroup
+  // ids go to the 8 XCDs round-robin in launch order; remap them so that each
+  // XCD runs whole splits (every tile of a contraction range), whose tiles
+  // read the same rows of both operands at the same time through its L2.
+  int bx = blockIdx.x, by = blockIdx.y;
+  if (gridDim.y > 1 && gridDim.y % 8 == 0) {
+    const int L = blockIdx.x + gridDim.x * blockIdx.y, x = L % 8, j = L / 8;
+    by = x * (gridDim.y / 8) + j / gridDim.x;
+    bx = j % gridDim.x;
+  }
+  const int64_t kbeg = (int64_t)by * g.k_split;
   const int64_t kend = kbeg + g.k_split < g.K ? kbeg + g.k_split : g.K;
   const int nsteps = kend > kbeg ? (int)((kend - kbeg + BK - 1) / BK) : 0;
   const int lrow = lane & 31, lhalf = lane >> 5;
@@ -783,7 +793,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
               *(float4*)(dst + 8 * b + 4 * lhalf) =
                   make_float4(acc[i][j][4 * b], acc[i][j][4 * b + 1], acc[i][j][4 * b + 2], acc[i][j][4 * b + 3]);
           } else {
-            float* part = (float*)g.C + (int64_t)blockIdx.y * g.M * g.N;
+            float* part = (float*)g.C + (int64_t)by * g.M * g.N;
             if (row < g.M) {
 #pragma unroll
               for (int b = 0; b < 4; ++b) {
@@ -798,7 +808,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     } else if constexpr (Cfg::EPI == EPI_F32) {
       // 2:4 products, split-K partial rows (layout as below): 32 lanes store
       // 32 consecutive columns of one row per accumulator.
-      float* part = (float*)g.C + (int64_t)blockIdx.y * g.M * g.N;
+      float* part = (float*)g.C + (int64_t)by * g.M * g.N;
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -1153,7 +1163,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     // tile, so its first loads are in flight during this tile's last steps
     // and epilogue.
     const TileRange tr = panels ? TileRange{(int)blockIdx.x / 8, (int)gridDim.x / 8, pm_count * pn_count}
-                                : tile_range(blockIdx.x, gridDim.x, ntiles);
+                                : tile_range(bx, gridDim.x, ntiles);
     if (tr.first >= tr.end) return;
     int tile = tr.first;
     int64_t m0, n0;
@@ -1447,7 +1457,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         it = (int64_t)t * S + k_last;
       }
     } else {
-      origin(xcd_remap(blockIdx.x, ntiles), m0, n0);
+      origin(xcd_remap(bx, ntiles), m0, n0);
       run_tile(m0, n0, kbeg, nsteps);
       epilogue(m0, n0, smem, [] {});
     }
