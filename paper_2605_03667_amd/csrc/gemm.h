@@ -1056,16 +1056,22 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       // (measured faster there, within its registers)
       int td = tid;
       if constexpr (Cfg::EPI == EPI_SPARSIFY) asm volatile("" : "+v"(td));
-      constexpr int VCH = BN * (BM / 16);
+      // Iteration it covers NT/4 token rows of one entry block: row
+      // (it % IPB) NT/4 + td/4, chunk td % 4 (LDS chunk position c ^ (row % 16)
+      // = X ^ 4 kb with X fixed per thread), global offset kb R 32 + row 32 +
+      // 8 (td % 4) = kb R 32 + (it % IPB) NT/4 32 + 8 td.
+      constexpr int RPI = NT / 4, IPB = BN / RPI;
+      static_assert(BN % RPI == 0 && BM == 256, "copy-out shape");
+      const int t0 = td >> 2, X = (td & 3) ^ (t0 & 15);
 #pragma unroll
-      for (int it = 0; it < VCH / NT; ++it) {
-        const int q = it * NT + td, kbi = q / (4 * BN), row = (q / 4) % BN, c = kbi * 4 + q % 4;
-        if (row < t_end && c * 16 < f_end) {
-          const uint32_t* sp = (const uint32_t*)(lv + row * BM + (c ^ (row & 15)) * 16);
+      for (int it = 0; it < IPB * (BM / 64); ++it) {
+        const int kb = it / IPB, rbase = (it % IPB) * RPI, row = rbase + t0;
+        if (row < t_end && kb * 64 < f_end) {
+          const uint32_t* sp = (const uint32_t*)(lv + row * BM + (X ^ (kb << 2)) * 16);
           // non-temporal: the compressed rows stream out and should not evict
           // the weight panel this XCD keeps in L2
           const u32x4 v = {sp[0], sp[1], sp[2], sp[3]};
-          __builtin_nontemporal_store(v, (u32x4*)(dst + kbi * Rb * 32 + row * 32 + (q % 4) * 8));
+          __builtin_nontemporal_store(v, (u32x4*)(dst + kb * Rb * 32 + rbase * 32 + td * 8));
         }
       }
       if constexpr (Cfg::EPI == EPI_SPARSIFY) {
