@@ -194,7 +194,9 @@ def table3_compare(iters: int = 20, warmup: int = 3) -> dict:
     which re-lays out the four factors on every call (one launch;
     `elas_weight_relayout_us` is that launch).  `fullrank_hipblaslt_us` times
     the same full-rank block built from torch.matmul (hipBLASLt) and torch
-    elementwise kernels, as a reference for the baseline's quality."""
+    elementwise kernels, as a reference for the baseline's quality.
+    `elas_fused_us` times the one-launch fused forward (ELAS_FWD_FUSED) where
+    the shape allows it (d <= 1024, r = 128 or 256), else null."""
     import numpy as np
     import torch
 
@@ -258,8 +260,9 @@ def table3_compare(iters: int = 20, warmup: int = 3) -> dict:
         ws = torch.empty(max(1, *(elas.elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r, fl)
                                   for T in TABLE3_SEQ for fl in (0, AB))), dtype=torch.uint8, device=dev)
         fab = {n: t[n].t().contiguous() for n in ("U_up", "V_up", "U_down", "V_down")}
-        row = {"elas_us": [], "elas_with_relayout_us": [], "fullrank_us": [], "fullrank_hipblaslt_us": [],
-               "speedup": [], "speedup_vs_best": []}
+        row = {"elas_us": [], "elas_with_relayout_us": [], "elas_fused_us": [], "fullrank_us": [],
+               "fullrank_hipblaslt_us": [], "speedup": [], "speedup_vs_best": []}
+        fused_ok = d % 64 == 0 and d <= 1024 and r in (128, 256)
         Wu_t, Wd_t = W_up.t(), W_down.t()
         for T in TABLE3_SEQ:
             x = t["x"][:T]
@@ -269,6 +272,11 @@ def table3_compare(iters: int = 20, warmup: int = 3) -> dict:
                                                             flags=AB, out=ol, workspace=ws))
             e_rl = device_us(lambda: elas.elas_lowrank_ffn_fwd(x, t["U_up"], t["V_up"], t["U_down"], t["V_down"],
                                                                out=ol, workspace=ws))
+            if fused_ok:
+                ef = device_us(lambda: elas.elas_lowrank_ffn_fwd(
+                    x, fab["U_up"], fab["V_up"], fab["U_down"], fab["V_down"], flags=AB | elas.ELAS_FWD_FUSED,
+                    out=ol, workspace=ws))
+                row["elas_fused_us"].append(round(ef, 2))
             f = device_us(lambda: elas.elas_fullrank_ffn_fwd(x, W_up, W_down, out=of))
             # the same block from the vendor GEMM library (torch.matmul -> hipBLASLt) and
             # torch elementwise kernels, as a reference for the full-rank time
@@ -291,6 +299,8 @@ def table3_compare(iters: int = 20, warmup: int = 3) -> dict:
         T = Tmax
         row["fullrank_tflops_at_max_T"] = round(4.0 * T * d * F / (row["fullrank_us"][-1] * 1e-6) / 1e12, 1)
         row["elas_alg_tflops_at_max_T"] = round(T * (4.0 * d * r + 3.0 * r * F) / (row["elas_us"][-1] * 1e-6) / 1e12, 1)
+        if not fused_ok:
+            row["elas_fused_us"] = None
         row["shape"] = {"d": d, "d_ff": F, "d_ff_true": c["d_ff_true"], "r": r}
         row["paper_speedup"] = TABLE3_PAPER[name]
         models[name] = row

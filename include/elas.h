@@ -101,6 +101,17 @@ extern "C" {
                                    the kernels' operand layout, so nothing is re-laid out (for
                                    inference with pre-arranged weights); results are identical */
 
+/* elas_lowrank_ffn_fwd only, sparse mode: launch shape.  Without either flag the library
+   picks.  Both compute the same block (Eq. 1-3, Algorithm 1) and write the same outputs in
+   the same layouts; their fp32 sums run in a different order, so results can differ in the
+   last bits (and a group whose ranking ties within that difference can keep another pair). */
+#define ELAS_FWD_FUSED      16u /* one launch per call: each workgroup computes P, S, Z and Y
+                                   for its block of tokens, with P and a d_ff chunk of S in LDS
+                                   and Z accumulated on chip (the fully fused forward).  Needs
+                                   d a multiple of 64 up to 1024 and r = 128 or 256, else
+                                   ELAS_ERR_SHAPE                                              */
+#define ELAS_FWD_UNFUSED    32u /* the four-kernel sequence (k1 .. k4)                         */
+
 /* elas_spmm_24: layout of the dense operand B. */
 #define ELAS_B_KN            0  /* B is [K x N] row-major                         */
 #define ELAS_B_NK            1  /* B is [N x K] row-major (B^T stored)            */

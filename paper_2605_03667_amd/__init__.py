@@ -23,7 +23,7 @@ __all__ = [
     "elas_lowrank_ffn_bwd", "elas_lowrank_ffn_bwd_workspace_bytes", "elas_fullrank_ffn_fwd",
     "elas_timing_enable", "elas_timing_collect",
     "ELAS_SPARSIFY_RELU2", "ELAS_SPARSIFY_RAW", "ELAS_B_KN", "ELAS_B_NK", "ELAS_MODE_SPARSE24",
-    "ELAS_MODE_DENSE", "ELAS_BWD_STE", "ELAS_FACTORS_AB",
+    "ELAS_MODE_DENSE", "ELAS_BWD_STE", "ELAS_FACTORS_AB", "ELAS_FWD_FUSED", "ELAS_FWD_UNFUSED",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libelas.so")
@@ -36,6 +36,8 @@ ELAS_MODE_SPARSE24 = 0
 ELAS_MODE_DENSE = 2
 ELAS_BWD_STE = 4
 ELAS_FACTORS_AB = 8
+ELAS_FWD_FUSED = 16
+ELAS_FWD_UNFUSED = 32
 
 _STATUS = {0: "ELAS_OK", 1: "ELAS_ERR_NULL", 2: "ELAS_ERR_SHAPE", 3: "ELAS_ERR_ALIGN",
            4: "ELAS_ERR_WORKSPACE", 5: "ELAS_ERR_FLAGS", 6: "ELAS_ERR_DEVICE"}

@@ -139,10 +139,17 @@ int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t
                          uint16_t* y, uint16_t* P, uint16_t* s_vals, uint8_t* s_meta, uint16_t* Z,
                          void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
-  if (flags & ~(ELAS_MODE_DENSE | ELAS_FACTORS_AB))
-    return fail(ELAS_ERR_FLAGS, "forward flags: only ELAS_MODE_DENSE and ELAS_FACTORS_AB are allowed");
+  if (flags & ~(ELAS_MODE_DENSE | ELAS_FACTORS_AB | ELAS_FWD_FUSED | ELAS_FWD_UNFUSED))
+    return fail(ELAS_ERR_FLAGS,
+                "forward flags: only ELAS_MODE_DENSE, ELAS_FACTORS_AB, ELAS_FWD_FUSED and ELAS_FWD_UNFUSED are allowed");
   const bool dense = (flags & ELAS_MODE_DENSE) != 0, ab = (flags & ELAS_FACTORS_AB) != 0;
+  const bool fused = (flags & ELAS_FWD_FUSED) != 0, unfused = (flags & ELAS_FWD_UNFUSED) != 0;
+  if (fused && unfused) return fail(ELAS_ERR_FLAGS, "ELAS_FWD_FUSED and ELAS_FWD_UNFUSED exclude each other");
+  if (fused && dense) return fail(ELAS_ERR_FLAGS, "ELAS_FWD_FUSED applies to the sparse forward only");
   ELAS_CHECK(check_ffn_dims(T, d, d_ff, r));
+  if (fused && !elas::fused_fwd_supported(d, r))
+    return fail(ELAS_ERR_SHAPE, "ELAS_FWD_FUSED needs d a multiple of 64 up to 1024 and r = 128 or 256 (d=%lld r=%lld)",
+                (long long)d, (long long)r);
   if (T == 0) return ELAS_OK;
   ELAS_CHECK(check_ptr(x, "x"));
   ELAS_CHECK(check_ptr(U_up, "U_up"));
@@ -165,6 +172,7 @@ int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t
   a.ws = workspace;
   a.dense = dense;
   a.ab = ab;
+  a.fused = fused ? 1 : unfused ? 2 : 0;
   return device_status(elas::run_fwd(a, (hipStream_t)stream), "forward launch");
 }
 

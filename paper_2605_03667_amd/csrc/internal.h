@@ -51,7 +51,15 @@ struct FfnArgs {
   bool dense;   // activations dense [T x d_ff] (no 2:4 selection)
   bool ste;     // backward: straight-through estimator through the selection
   bool ab;      // forward: factors given as U_up^T, V_up^T, U_down^T, V_down^T
+  int fused;    // sparse forward: 0 the library picks, 1 one fused launch, 2 four kernels
 };
+
+// fused.hip: the one-launch sparse forward for compact factor shapes
+bool fused_fwd_supported(int64_t d, int64_t r);
+hipError_t run_fused_fwd(const uint16_t* x, const uint16_t* U_upT, const uint16_t* V_upT, const uint16_t* U_downT,
+                         const uint16_t* V_downT, int64_t T, int64_t d, int64_t F, int64_t r, int64_t F_rows,
+                         int64_t ld_ud, uint16_t* y, uint16_t* P, uint16_t* s_vals, uint8_t* s_meta, uint16_t* Z,
+                         hipStream_t stream);
 
 // ffn.hip
 size_t spmm_workspace_bytes(int64_t K, int64_t N, int b_layout);

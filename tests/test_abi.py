@@ -109,7 +109,11 @@ def test_fwd_validation():
     L = elas.lib()
     assert _fwd(L, flags=1) == 5
     assert _fwd(L, flags=4) == 5                # STE is a backward-only flag
-    assert _fwd(L, flags=16) == 5
+    assert _fwd(L, flags=64) == 5
+    assert _fwd(L, flags=16 | 32) == 5         # fused and unfused at once
+    assert _fwd(L, flags=16 | 2) == 5          # the fused forward is sparse-mode only
+    assert _fwd(L, flags=16) == 2              # d = 32, r = 16: no fused kernel for that shape
+    assert _fwd(L, d=64, r=128, flags=16) == 1  # supported shape: on to the pointer checks (x is fake, y fine)
     # pre-arranged factors need no factor copies in the workspace
     assert (L.elas_lowrank_ffn_fwd_workspace_bytes(65536, 2048, 5464, 512, 8)
             < L.elas_lowrank_ffn_fwd_workspace_bytes(65536, 2048, 5464, 512, 0))
