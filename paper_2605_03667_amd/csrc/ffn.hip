@@ -423,7 +423,11 @@ hipError_t gemm_nt_bf16(const char* tag, const uint16_t* A, int64_t lda, const u
 
 // Work split of a K = T product.  Split-K: enough workgroups to cover the 256
 // CUs once, each split at least 8 K steps long (more splits fill the CUs more
-// evenly but cost more partial-sum traffic than they save at the 1B shapes).
+// evenly but cost more partial-sum traffic than they save at the 1B shapes);
+// below 16 steps (T < 1024) and for outputs under 2^20 elements, splits may be
+// 2 steps long, since there the latency of a few long workgroups dominates
+// (measured: the 60M backward at 512 tokens 134 -> 93 us; the same rule was
+// slower at 2048 tokens and above, and for the 1B shape's larger outputs).
 // When that leaves more than a tenth of the CUs idle, the register-staged
 // (2:4) products use stream-K instead: 256 workgroups with equal shares of
 // the tiles x K steps, each at least 8 steps.
@@ -440,9 +444,10 @@ struct SplitPlan {
 SplitPlan plan_tiles(int64_t M, int64_t N, int64_t K, int tb) {
   const int64_t tiles = cdiv(M, tb) * cdiv(N, tb);
   const int64_t steps = cdiv(K, 64);
+  const int64_t min_steps = steps < 16 && M * N < (1 << 20) ? 2 : 8;
   int64_t s = 256 / tiles;
   if (s < 1) s = 1;
-  if (s > steps / 8) s = steps / 8 > 0 ? steps / 8 : 1;
+  if (s > steps / min_steps) s = steps / min_steps > 0 ? steps / min_steps : 1;
   const int64_t k_split = cdiv(cdiv(K, s), 64) * 64;
   return {(int)cdiv(K, k_split), k_split, 0, 0, tb == 128};
 }
