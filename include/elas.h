@@ -254,8 +254,12 @@ int elas_fullrank_ffn_fwd(const uint16_t* x, const uint16_t* W_up, const uint16_
  * kernel tag; it returns the number of tags (or -ELAS_ERR_DEVICE).
  * elas_timing_entry(i, ...) returns tag i's name (NUL-terminated, truncated to
  * name_cap), its number of launches and their summed duration in ms.
+ * elas_timing_only(tag) restricts recording to the launches of one kernel tag
+ * (the string is copied), so that a timed region carries only that kernel's
+ * events; NULL or "" restores recording of every launch.  Always ELAS_OK.
  */
 int elas_timing_enable(int enable);
+int elas_timing_only(const char* tag);
 int elas_timing_collect(void);
 int elas_timing_entry(int i, char* name, int name_cap, int64_t* launches, double* total_ms);
 

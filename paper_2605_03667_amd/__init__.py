@@ -21,7 +21,7 @@ __all__ = [
     "ElasError", "lib", "elas_vals_ld", "elas_meta_ld", "elas_sparsify_24", "elas_spmm_24",
     "elas_spmm_24_workspace_bytes", "elas_lowrank_ffn_fwd", "elas_lowrank_ffn_fwd_workspace_bytes",
     "elas_lowrank_ffn_bwd", "elas_lowrank_ffn_bwd_workspace_bytes", "elas_fullrank_ffn_fwd",
-    "elas_timing_enable", "elas_timing_collect",
+    "elas_timing_enable", "elas_timing_only", "elas_timing_collect",
     "ELAS_SPARSIFY_RELU2", "ELAS_SPARSIFY_RAW", "ELAS_B_KN", "ELAS_B_NK", "ELAS_MODE_SPARSE24",
     "ELAS_MODE_DENSE", "ELAS_BWD_STE", "ELAS_FACTORS_AB", "ELAS_FWD_FUSED", "ELAS_FWD_UNFUSED",
 ]
@@ -71,6 +71,7 @@ _SIGNATURES = {
                              ctypes.c_int),
     "elas_fullrank_ffn_fwd": ([_p] * 3 + [_i64] * 3 + [_p] * 3, ctypes.c_int),
     "elas_timing_enable": ([ctypes.c_int], ctypes.c_int),
+    "elas_timing_only": ([ctypes.c_char_p], ctypes.c_int),
     "elas_timing_collect": ([], ctypes.c_int),
     "elas_timing_entry": ([ctypes.c_int, ctypes.c_char_p, ctypes.c_int, ctypes.POINTER(_i64),
                            ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
@@ -265,6 +266,11 @@ def elas_fullrank_ffn_fwd(x, W_up, W_down, out: dict | None = None) -> dict:
 def elas_timing_enable(enable: bool = True) -> None:
     """Start (clearing earlier records) or stop per-kernel event timing."""
     _check(lib().elas_timing_enable(1 if enable else 0))
+
+
+def elas_timing_only(tag: str | None = None) -> None:
+    """Record only the launches of kernel ``tag`` (None: every launch)."""
+    _check(lib().elas_timing_only(tag.encode() if tag else None))
 
 
 def elas_timing_collect() -> dict:

@@ -25,6 +25,7 @@ struct Entry {
 };
 
 bool g_enabled = false;
+std::string g_only;                   // when not empty: the one tag that is timed
 std::vector<hipEvent_t> g_pool;       // every event ever created, reused
 size_t g_next = 0;                    // next free event in g_pool
 std::vector<Record> g_records;
@@ -44,7 +45,7 @@ hipEvent_t next_event() {
 bool timing_enabled() { return g_enabled; }
 
 TimedLaunch::TimedLaunch(const char* tag, hipStream_t stream) : tag_(tag), stream_(stream) {
-  if (!g_enabled) return;
+  if (!g_enabled || (!g_only.empty() && g_only != tag)) return;
   start_ = next_event();
   stop_ = next_event();
   if (start_ && stop_) hipEventRecord(start_, stream_);
@@ -67,6 +68,11 @@ int elas_timing_enable(int enable) {
     elas::g_entries.clear();
     elas::g_next = 0;
   }
+  return ELAS_OK;
+}
+
+int elas_timing_only(const char* tag) {
+  elas::g_only = tag ? tag : "";
   return ELAS_OK;
 }
 

@@ -32,7 +32,7 @@ def _defines():
 
 def test_exports_every_declared_symbol():
     names = _declared()
-    assert len(names) == 15, names
+    assert len(names) == 16, names
     lib = ctypes.CDLL(elas.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -182,3 +182,12 @@ def test_tiled_layout_helpers():
                     flat[index(t, j, T, ld, bw)] = a[t, j]
             assert np.array_equal(tile(a, bw), flat)
             assert np.array_equal(untile(flat.reshape(T, ld), T, ld, bw), a)
+
+
+def test_timing_filter_is_host_only():
+    """elas_timing_only touches no device: it can be set and cleared on CPU."""
+    L = elas.lib()
+    assert L.elas_timing_only(b"b3_dH_masked") == 0
+    assert L.elas_timing_only(None) == 0
+    assert L.elas_timing_only(b"") == 0
+
