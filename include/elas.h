@@ -101,8 +101,9 @@ extern "C" {
                                    the kernels' operand layout, so nothing is re-laid out (for
                                    inference with pre-arranged weights); results are identical */
 
-/* elas_lowrank_ffn_fwd only, sparse mode: launch shape.  Without either flag the library
-   picks.  Both compute the same block (Eq. 1-3, Algorithm 1) and write the same outputs in
+/* elas_lowrank_ffn_fwd only, sparse mode: launch shape.  Without either flag the forward is
+   the four-kernel sequence (on MI355X faster than the fused launch at every supported shape
+   but one).  Both compute the same block (Eq. 1-3, Algorithm 1) and write the same outputs in
    the same layouts; their fp32 sums run in a different order, so results can differ in the
    last bits (and a group whose ranking ties within that difference can keep another pair). */
 #define ELAS_FWD_FUSED      16u /* one launch per call: each workgroup computes P, S, Z and Y

@@ -613,12 +613,6 @@ hipError_t run_spmm24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, 
   return launch_sp("spmm24", g, st);
 }
 
-// Whether the library's default for the sparse forward is the fused launch.
-static bool fused_fwd_auto(int64_t T, int64_t d, int64_t F, int64_t r) {
-  (void)T; (void)F;
-  return false && fused_fwd_supported(d, r);
-}
-
 hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
   const int64_t T = a.T, d = a.d, F = a.F, r = a.r, Fp = pad64(F);
   const FwdWs w = fwd_ws((char*)a.ws, T, d, F, r, a.ab);
@@ -638,7 +632,9 @@ hipError_t run_fwd(const FfnArgs& a, hipStream_t st) {
     F_rows = Fp;
     ld_ud = Fp;
   }
-  if (!a.dense && (a.fused == 1 || (a.fused == 0 && fused_fwd_auto(T, d, F, r))))
+  // The one-launch forward only on request: measured slower than the four
+  // kernels below at every supported shape but one.
+  if (!a.dense && a.fused == 1)
     return run_fused_fwd(a.x, U_upT, V_upT, U_downT, V_downT, T, d, F, r, F_rows, ld_ud, a.y, a.P, a.s_vals,
                          a.s_meta, a.Z, st);
   // P = x U_up

@@ -51,7 +51,7 @@ struct FfnArgs {
   bool dense;   // activations dense [T x d_ff] (no 2:4 selection)
   bool ste;     // backward: straight-through estimator through the selection
   bool ab;      // forward: factors given as U_up^T, V_up^T, U_down^T, V_down^T
-  int fused;    // sparse forward: 0 the library picks, 1 one fused launch, 2 four kernels
+  int fused;    // sparse forward: 1 one fused launch, else (0 default, 2 requested) four kernels
 };
 
 // fused.hip: the one-launch sparse forward for compact factor shapes
