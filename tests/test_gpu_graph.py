@@ -15,14 +15,17 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("name,T", [(None, 300), ("llama1b", 512)])
-@pytest.mark.parametrize("mode", ["sparse", "dense", "ste"])
+@pytest.mark.parametrize("mode", ["sparse", "dense", "ste", "fused"])
 def test_graph_replays_match_eager(name, T, mode):
-    bits = config_inputs(name, T=T) if name else ffn_inputs(T, 128, 264, 32, seed_base=9)
+    if mode == "fused":   # the fused forward's shapes: r = 128 (the 60M model instead of 1B)
+        bits = config_inputs("llama60m", T=T) if name else ffn_inputs(T, 128, 264, 128, seed_base=9)
+    else:
+        bits = config_inputs(name, T=T) if name else ffn_inputs(T, 128, 264, 32, seed_base=9)
     t = {k: dev_bf16(v) for k, v in bits.items()}
     T, d = bits["x"].shape
     r, F = bits["V_up"].shape
-    fflags = elas.ELAS_MODE_DENSE if mode == "dense" else 0
-    bflags = {"sparse": 0, "ste": elas.ELAS_BWD_STE, "dense": elas.ELAS_MODE_DENSE}[mode]
+    fflags = {"sparse": 0, "ste": 0, "dense": elas.ELAS_MODE_DENSE, "fused": elas.ELAS_FWD_FUSED}[mode]
+    bflags = {"sparse": 0, "ste": elas.ELAS_BWD_STE, "dense": elas.ELAS_MODE_DENSE, "fused": 0}[mode]
     saved = elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], flags=fflags)
     grads = elas.elas_lowrank_ffn_bwd(t["dY"], t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], saved,
                                       flags=bflags)
