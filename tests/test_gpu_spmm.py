@@ -69,3 +69,17 @@ def test_zero_rows_is_noop():
                           torch.zeros((N, K), dtype=torch.bfloat16, device="cuda:0"), elas.ELAS_B_NK)
     torch.cuda.synchronize()
     assert c.shape == (0, N)
+
+
+def _random_shapes(n, seed):
+    g = np.random.default_rng(seed)
+    return [(int(g.integers(1, 1200)), 8 * int(g.integers(1, 400)), 8 * int(g.integers(1, 80))) for _ in range(n)]
+
+
+@pytest.mark.parametrize("layout", [elas.ELAS_B_NK, elas.ELAS_B_KN])
+@pytest.mark.parametrize("M,K,N", _random_shapes(10, 2026))
+def test_random_shapes_exact(M, K, N, layout):
+    """Seeded random M (any), K and N (multiples of 8): bit-exact on small integers."""
+    vals, meta, b, ref = _operands(M, K, N, M + 3 * K + N, exact=True)
+    got = _gpu(vals, meta, b, K, layout)
+    np.testing.assert_array_equal(got, obf.from_f64(ref))
