@@ -105,7 +105,8 @@ extern "C" {
    the four-kernel sequence (on MI355X faster than the fused launch at every supported shape
    but one).  Both compute the same block (Eq. 1-3, Algorithm 1) and write the same outputs in
    the same layouts; their fp32 sums run in a different order, so results can differ in the
-   last bits (and a group whose ranking ties within that difference can keep another pair). */
+   last bits (and a group whose ranking ties within that difference can keep another pair).
+   Both flags together, or ELAS_FWD_FUSED with ELAS_MODE_DENSE: ELAS_ERR_FLAGS. */
 #define ELAS_FWD_FUSED      16u /* one launch per call: each workgroup computes P, S, Z and Y
                                    for its block of tokens, with P and a d_ff chunk of S in LDS
                                    and Z accumulated on chip (the fully fused forward).  Needs
