@@ -46,18 +46,22 @@ def _rounder(bf16io: bool):
     return bf16.round_f64 if bf16io else (lambda a: a)
 
 
-def forward(x, U_up, V_up, U_down, V_down, *, bf16io: bool = True, sparse: bool = True):
+def forward(x, U_up, V_up, U_down, V_down, *, bf16io: bool = True, sparse: bool = True, mask=None):
     """Forward pass.  Inputs are float64 arrays (exact bf16 values).
 
     Returns a dict with Y and the intermediates P, H, s, mask, S, Z.
     ``sparse=False`` skips Algorithm 1 (dense activations, the paper's
-    warm-up phase).
+    warm-up phase).  ``mask`` (boolean, H's shape) replaces Algorithm 1's
+    selection by a given one, e.g. the selection of the bf16-rounded block
+    applied to the plain float64 block, so that the two differ only in
+    their arithmetic.
     """
     rb = _rounder(bf16io)
     P = rb(x @ U_up)
     H = rb(P @ V_up)
     s = relu2(H)
-    mask = top2_mask(s) if sparse else np.ones(s.shape, dtype=bool)
+    if mask is None:
+        mask = top2_mask(s) if sparse else np.ones(s.shape, dtype=bool)
     S = rb(np.where(mask, s, 0.0))
     Z = rb(S @ U_down)
     Y = rb(Z @ V_down)
@@ -102,12 +106,12 @@ def from_bits(inputs: dict) -> dict:
     return {k: bf16.to_f64(v) for k, v in inputs.items()}
 
 
-def run(inputs_bits: dict, *, bf16io: bool = True, ste: bool = False, sparse: bool = True):
+def run(inputs_bits: dict, *, bf16io: bool = True, ste: bool = False, sparse: bool = True, mask=None):
     """Forward + backward on a dict of bf16 bit arrays (x, U_up, V_up, U_down,
     V_down, dY).  Returns (forward dict, backward dict)."""
     a = from_bits(inputs_bits)
     f = forward(a["x"], a["U_up"], a["V_up"], a["U_down"], a["V_down"],
-                bf16io=bf16io, sparse=sparse)
+                bf16io=bf16io, sparse=sparse, mask=mask)
     b = backward(a["dY"], a["x"], a["U_up"], a["V_up"], a["U_down"], a["V_down"], f,
                  bf16io=bf16io, ste=ste)
     return f, b

@@ -77,6 +77,27 @@ def ffn_inputs(T: int, d: int, d_ff: int, r: int, d_ff_true: int | None = None,
     return out
 
 
+def exact_p_inputs(T: int, d: int, d_ff: int, r: int, d_ff_true: int | None = None,
+                   seed_base: int = 0) -> dict:
+    """Like ffn_inputs, but x and U_up are drawn on coarse grids so that
+    every sum of x U_up is exact in binary32 (and float64): x ~ N(0, 1) on
+    multiples of 1/8 in [-4, 4] (at most 6 significant bits), U_up ~ N(0, 1/d)
+    on multiples of 2^-g, g = floor(log2(64 sqrt(d))), at most 255 grid steps
+    (8 bits).  Both are exact bf16 values, so every implementation that
+    accumulates in binary32 holds the same P, and differences downstream come
+    from the later products only.  The other tensors are those of
+    ffn_inputs."""
+    out = ffn_inputs(T, d, d_ff, r, d_ff_true, seed_base)
+    s = 1000 * seed_base
+    g = _rng(s + 7)
+    x = np.clip(np.rint(g.standard_normal((T, d)) * 8.0), -32, 32) / 8.0
+    step = 2.0 ** -int(np.floor(np.log2(64.0 * np.sqrt(d))))
+    u = np.clip(np.rint(g.standard_normal((d, r)) / np.sqrt(d) / step), -255, 255) * step
+    out["x"] = (x.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    out["U_up"] = (u.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    return out
+
+
 def fullrank_inputs(T: int, d: int, d_ff: int, d_ff_true: int | None = None, seed_base: int = 0) -> dict:
     """Inputs of the full-rank ReLU^2 FFN forward, as bf16 bits.
 
@@ -134,4 +155,14 @@ def uniform_int_bf16(shape, lo: int, hi: int, seed: int, scale_log2: int = 0) ->
     """
     g = _rng(seed)
     v = g.integers(lo, hi + 1, size=shape).astype(np.float32) * np.float32(2.0 ** scale_log2)
+    return (v.view(np.uint32) >> 16).astype(np.uint16)
+
+
+def sparse_sign_bf16(shape, density: float, seed: int, scale_log2: int = 0) -> np.ndarray:
+    """+-2**scale_log2 at a random fraction ``density`` of the positions, 0
+    elsewhere, as bf16 bits.  Sparse small integers keep every sum of the
+    block exact in binary32 even at the largest model shape."""
+    g = _rng(seed)
+    v = np.where(g.random(shape) < density, g.choice(np.array([-1.0, 1.0]), size=shape), 0.0)
+    v = (v * 2.0 ** scale_log2).astype(np.float32)
     return (v.view(np.uint32) >> 16).astype(np.uint16)
