@@ -31,7 +31,7 @@ def _shapes(n, seed):
 def test_random_shapes(T, d, F, r, mode):
     bits = ffn_inputs(T, d, F, r, seed_base=T + d + F + r)
     f, b = offn.run(bits, sparse=(mode != "dense"), ste=(mode == "ste"))
-    compare(run_gpu(bits, mode=mode), f, b)
+    compare(run_gpu(bits, mode=mode), f, b, bits, mode=mode)
 
 
 def _fused_shapes(n, seed):
@@ -44,4 +44,4 @@ def _fused_shapes(n, seed):
 def test_random_shapes_fused(T, d, F, r):
     bits = ffn_inputs(T, d, F, r, seed_base=T + d + F + r + 1)
     f, b = offn.run(bits)
-    compare(run_gpu(bits, fwd_flags=elas.ELAS_FWD_FUSED), f, b)
+    compare(run_gpu(bits, fwd_flags=elas.ELAS_FWD_FUSED), f, b, bits)

@@ -83,3 +83,16 @@ def test_random_shapes_exact(M, K, N, layout):
     vals, meta, b, ref = _operands(M, K, N, M + 3 * K + N, exact=True)
     got = _gpu(vals, meta, b, K, layout)
     np.testing.assert_array_equal(got, obf.from_f64(ref))
+
+
+@pytest.mark.parametrize("M,K,N", [(24832, 2736, 512), (49408, 5464, 256)])
+def test_exact_persistent_256_tiles(M, K, N):
+    """M large enough for at least 192 tiles of 256 x 256, so the product runs
+    the persistent 256 x 256 smfmac configuration on the row-layout 2:4
+    operand (smaller problems take 128 x 128 tiles): bit-exact on small
+    integers in both layouts of B."""
+    vals, meta, b, ref = _operands(M, K, N, M + K + N, exact=True)
+    want = obf.from_f64(ref)
+    for layout in (elas.ELAS_B_NK, elas.ELAS_B_KN):
+        got = _gpu(vals, meta, b, K, layout)
+        np.testing.assert_array_equal(got, want, err_msg=f"layout {layout}")
