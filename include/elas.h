@@ -21,7 +21,8 @@
  * - Dense tensors are row-major and contiguous.  Every pointer must be 16-byte
  *   aligned.
  * - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
- *   work is enqueued on it asynchronously; the calls do not synchronise.
+ *   work is enqueued on it asynchronously; the calls do not synchronise
+ *   (except in the debug mode, elas_debug_sync below).
  * - Arguments are validated on the host before anything is enqueued.  On an
  *   error nothing is launched, outputs are untouched, the return value is the
  *   error code and elas_last_error() (thread-local) describes it.  A failed
@@ -245,6 +246,34 @@ int elas_lowrank_ffn_bwd(const uint16_t* dy, const uint16_t* x, const uint16_t* 
  */
 int elas_fullrank_ffn_fwd(const uint16_t* x, const uint16_t* W_up, const uint16_t* W_down,
                           int64_t T, int64_t d, int64_t d_ff, uint16_t* y, uint16_t* S, void* stream);
+
+/*
+ * elas_meta_to_canonical / elas_vals_to_canonical -- read back the compressed
+ * S that elas_lowrank_ffn_fwd saves (tiled layout above; the storage of the
+ * kept values plus index information of Sec. 4.2.2) in the canonical form:
+ * row i's N/8 metadata bytes (resp. N/2 kept values) contiguous, no padding,
+ * group j's code in byte j/2 as in the row layout.
+ * HOST memory on both sides (copy the device buffers to the host first):
+ *   meta_tiled [M x elas_meta_ld(N)] bytes -> meta_canonical [M x N/8] bytes;
+ *   vals_tiled [M x elas_vals_ld(N)] bf16  -> vals_canonical [M x N/2] bf16.
+ * Requires M >= 0, N > 0, N % 8 == 0, N <= 65536; M == 0 is a no-op.  NULL
+ * buffers give ELAS_ERR_NULL.  Synchronous; no device work.
+ */
+int elas_meta_to_canonical(const uint8_t* meta_tiled, int64_t M, int64_t N, uint8_t* meta_canonical);
+int elas_vals_to_canonical(const uint16_t* vals_tiled, int64_t M, int64_t N, uint16_t* vals_canonical);
+
+/*
+ * Debug mode (ELAS_DEBUG_SYNC).  When on, every kernel an entry point
+ * launches is followed by a synchronisation of the caller's stream, and a
+ * failure is returned by that entry point as ELAS_ERR_DEVICE naming the
+ * kernel (elas_last_error), instead of surfacing at the caller's next
+ * synchronisation.  For debugging only: it serialises host and device and
+ * must not be used while the stream is being captured into a graph.
+ * The initial state is on when the environment variable ELAS_DEBUG_SYNC is
+ * set to anything but "0" at load time.  elas_debug_sync(1 / 0) switches it
+ * on / off, elas_debug_sync(-1) leaves it; each returns the previous state.
+ */
+int elas_debug_sync(int enable);
 
 /*
  * Per-kernel timing (diagnostics for benchmarks; not thread-safe).

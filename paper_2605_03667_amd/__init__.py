@@ -21,7 +21,8 @@ __all__ = [
     "ElasError", "lib", "elas_vals_ld", "elas_meta_ld", "elas_sparsify_24", "elas_spmm_24",
     "elas_spmm_24_workspace_bytes", "elas_lowrank_ffn_fwd", "elas_lowrank_ffn_fwd_workspace_bytes",
     "elas_lowrank_ffn_bwd", "elas_lowrank_ffn_bwd_workspace_bytes", "elas_fullrank_ffn_fwd",
-    "elas_timing_enable", "elas_timing_only", "elas_timing_collect",
+    "elas_timing_enable", "elas_timing_only", "elas_timing_collect", "elas_meta_to_canonical",
+    "elas_vals_to_canonical", "elas_debug_sync",
     "ELAS_SPARSIFY_RELU2", "ELAS_SPARSIFY_RAW", "ELAS_B_KN", "ELAS_B_NK", "ELAS_MODE_SPARSE24",
     "ELAS_MODE_DENSE", "ELAS_BWD_STE", "ELAS_FACTORS_AB", "ELAS_FWD_FUSED", "ELAS_FWD_UNFUSED",
 ]
@@ -41,6 +42,9 @@ ELAS_FWD_UNFUSED = 32
 
 _STATUS = {0: "ELAS_OK", 1: "ELAS_ERR_NULL", 2: "ELAS_ERR_SHAPE", 3: "ELAS_ERR_ALIGN",
            4: "ELAS_ERR_WORKSPACE", 5: "ELAS_ERR_FLAGS", 6: "ELAS_ERR_DEVICE"}
+
+
+_STATUS_CODE = {v: k for k, v in _STATUS.items()}
 
 
 class ElasError(RuntimeError):
@@ -70,6 +74,9 @@ _SIGNATURES = {
     "elas_lowrank_ffn_bwd": ([_p] * 6 + [_i64] * 4 + [_u32] + [_p] * 4 + [_p] * 5 + [_p, _sz, _p],
                              ctypes.c_int),
     "elas_fullrank_ffn_fwd": ([_p] * 3 + [_i64] * 3 + [_p] * 3, ctypes.c_int),
+    "elas_meta_to_canonical": ([_p, _i64, _i64, _p], ctypes.c_int),
+    "elas_vals_to_canonical": ([_p, _i64, _i64, _p], ctypes.c_int),
+    "elas_debug_sync": ([ctypes.c_int], ctypes.c_int),
     "elas_timing_enable": ([ctypes.c_int], ctypes.c_int),
     "elas_timing_only": ([ctypes.c_char_p], ctypes.c_int),
     "elas_timing_collect": ([], ctypes.c_int),
@@ -96,6 +103,17 @@ def lib() -> ctypes.CDLL:
 def _check(rc: int) -> None:
     if rc != 0:
         raise ElasError(rc, lib().elas_last_error().decode())
+
+
+def _shape(t: torch.Tensor | None, shape: tuple, name: str) -> None:
+    """Raise unless tensor ``t`` has exactly ``shape``: the C ABI receives bare
+    pointers and cannot check the size of a buffer, so a tensor of the wrong
+    size would be read or written out of bounds.  Runs before any pointer is
+    taken, so a wrong size is reported whatever the tensor's device."""
+    if t is None:
+        raise ValueError(f"{name} is required (shape {tuple(shape)})")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
 
 
 def _ptr(t: torch.Tensor | None, dtype: torch.dtype, name: str):
@@ -136,6 +154,8 @@ def elas_sparsify_24(h: torch.Tensor, flags: int = ELAS_SPARSIFY_RELU2, vals: to
         vals = torch.empty((M, elas_vals_ld(N)), dtype=torch.bfloat16, device=h.device)
     if meta is None:
         meta = torch.empty((M, elas_meta_ld(N)), dtype=torch.uint8, device=h.device)
+    _shape(vals, (M, elas_vals_ld(N)), "vals")
+    _shape(meta, (M, elas_meta_ld(N)), "meta")
     _check(lib().elas_sparsify_24(_ptr(h, torch.bfloat16, "h"), M, N, flags,
                                   _ptr(vals, torch.bfloat16, "vals"), _ptr(meta, torch.uint8, "meta"),
                                   _stream(h.device)))
@@ -152,9 +172,15 @@ def elas_spmm_24(a_vals: torch.Tensor, a_meta: torch.Tensor, K: int, b: torch.Te
     """C [M, N] = A B with A 2:4-compressed [M, K] (vals, meta) and B [K, N]
     (ELAS_B_KN) or [N, K] (ELAS_B_NK)."""
     M = a_vals.shape[0]
+    if b.dim() != 2 or a_vals.dim() != 2:
+        raise ValueError("a_vals and b must be 2-D")
     N = b.shape[1] if b_layout == ELAS_B_KN else b.shape[0]
+    _shape(a_vals, (M, elas_vals_ld(K)), "a_vals")
+    _shape(a_meta, (M, elas_meta_ld(K)), "a_meta")
+    _shape(b, (K, N) if b_layout == ELAS_B_KN else (N, K), "b")
     if c is None:
         c = torch.empty((M, N), dtype=torch.bfloat16, device=a_vals.device)
+    _shape(c, (M, N), "c")
     need = elas_spmm_24_workspace_bytes(M, K, N, b_layout)
     if workspace is None:
         workspace = _workspace(need, a_vals.device)
@@ -163,6 +189,21 @@ def elas_spmm_24(a_vals: torch.Tensor, a_meta: torch.Tensor, K: int, b: torch.Te
                               _ptr(workspace, torch.uint8, "workspace"),
                               0 if workspace is None else workspace.numel(), _stream(a_vals.device)))
     return c
+
+
+def _saved_shapes(saved: dict, T: int, d: int, F: int, r: int, dense: bool, with_y: bool) -> None:
+    """Shapes of the forward's outputs (the backward's saved inputs) for the
+    activation mode: dense s_vals [T, d_ff]; compressed s_vals
+    [T, elas_vals_ld(d_ff)] and s_meta [T, elas_meta_ld(d_ff)]."""
+    if with_y:
+        _shape(saved.get("y"), (T, d), "y")
+    _shape(saved.get("P"), (T, r), "P")
+    _shape(saved.get("Z"), (T, r), "Z")
+    if dense:
+        _shape(saved.get("s_vals"), (T, F), "s_vals (dense mode)")
+    else:
+        _shape(saved.get("s_vals"), (T, elas_vals_ld(F)), "s_vals (2:4 mode)")
+        _shape(saved.get("s_meta"), (T, elas_meta_ld(F)), "s_meta (2:4 mode)")
 
 
 def elas_lowrank_ffn_fwd_workspace_bytes(T: int, d: int, d_ff: int, r: int, flags: int = 0) -> int:
@@ -188,6 +229,9 @@ def elas_lowrank_ffn_fwd(x, U_up, V_up, U_down, V_down, flags: int = 0, out: dic
     F = V_up.shape[0] if ab else V_up.shape[1]
     dev = x.device
     dense = bool(flags & ELAS_MODE_DENSE)
+    for t, shp, name in ((U_up, (d, r), "U_up"), (V_up, (r, F), "V_up"), (U_down, (F, r), "U_down"),
+                         (V_down, (r, d), "V_down")):
+        _shape(t, shp[::-1] if ab else shp, name)
     if out is None:
         out = {
             "y": torch.empty((T, d), dtype=torch.bfloat16, device=dev),
@@ -196,6 +240,7 @@ def elas_lowrank_ffn_fwd(x, U_up, V_up, U_down, V_down, flags: int = 0, out: dic
             "s_meta": None if dense else torch.empty((T, elas_meta_ld(F)), dtype=torch.uint8, device=dev),
             "Z": torch.empty((T, r), dtype=torch.bfloat16, device=dev),
         }
+    _saved_shapes(out, T, d, F, r, dense, with_y=True)
     need = elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r, flags)
     if workspace is None:
         workspace = _workspace(need, dev)
@@ -221,6 +266,10 @@ def elas_lowrank_ffn_bwd(dy, x, U_up, V_up, U_down, V_down, saved: dict, flags: 
     r = U_up.shape[1]
     F = V_up.shape[1]
     dev = x.device
+    for t, shp, name in ((dy, (T, d), "dy"), (U_up, (d, r), "U_up"), (V_up, (r, F), "V_up"),
+                         (U_down, (F, r), "U_down"), (V_down, (r, d), "V_down")):
+        _shape(t, shp, name)
+    _saved_shapes(saved, T, d, F, r, bool(flags & ELAS_MODE_DENSE), with_y=False)
     if grads is None:
         f32 = torch.float32
         grads = {
@@ -230,6 +279,8 @@ def elas_lowrank_ffn_bwd(dy, x, U_up, V_up, U_down, V_down, saved: dict, flags: 
             "dU_down": torch.empty((F, r), dtype=f32, device=dev),
             "dV_down": torch.empty((r, d), dtype=f32, device=dev),
         }
+    for k, shp in (("dx", (T, d)), ("dU_up", (d, r)), ("dV_up", (r, F)), ("dU_down", (F, r)), ("dV_down", (r, d))):
+        _shape(grads.get(k), shp, k)
     need = elas_lowrank_ffn_bwd_workspace_bytes(T, d, F, r, flags)
     if workspace is None:
         workspace = _workspace(need, dev)
@@ -253,14 +304,62 @@ def elas_fullrank_ffn_fwd(x, W_up, W_down, out: dict | None = None) -> dict:
     T, d = x.shape
     F = W_up.shape[0]
     dev = x.device
+    _shape(W_up, (F, d), "W_up")
+    _shape(W_down, (d, F), "W_down")
     if out is None:
         out = {"y": torch.empty((T, d), dtype=torch.bfloat16, device=dev),
                "S": torch.empty((T, F), dtype=torch.bfloat16, device=dev)}
+    _shape(out.get("y"), (T, d), "y")
+    _shape(out.get("S"), (T, F), "S")
     bf = torch.bfloat16
     _check(lib().elas_fullrank_ffn_fwd(
         _ptr(x, bf, "x"), _ptr(W_up, bf, "W_up"), _ptr(W_down, bf, "W_down"), T, d, F,
         _ptr(out["y"], bf, "y"), _ptr(out["S"], bf, "S"), _stream(dev)))
     return out
+
+
+def _host_array(a, dtype, shape, name):
+    """A C-contiguous host numpy array of ``dtype`` and ``shape`` from a numpy
+    array or a (host or device) torch tensor of the same element size."""
+    import numpy as np
+    if isinstance(a, torch.Tensor):
+        a = a.detach().contiguous().cpu().numpy()
+    a = np.ascontiguousarray(a)
+    if a.dtype.itemsize != np.dtype(dtype).itemsize:
+        raise ValueError(f"{name} must have {np.dtype(dtype).itemsize}-byte elements")
+    a = a.view(dtype)
+    if a.shape != tuple(shape):
+        raise ValueError(f"{name} has shape {a.shape}, expected {tuple(shape)}")
+    return a
+
+
+def elas_meta_to_canonical(meta_tiled, M: int, N: int):
+    """Canonical metadata [M, N/8] (uint8 numpy) of a compressed S saved by
+    elas_lowrank_ffn_fwd in the tiled layout ([M, elas_meta_ld(N)] bytes;
+    numpy or torch, copied to the host)."""
+    import numpy as np
+    src = _host_array(meta_tiled, np.uint8, (M, elas_meta_ld(N)), "meta_tiled")
+    out = np.empty((M, N // 8), dtype=np.uint8)
+    _check(lib().elas_meta_to_canonical(src.ctypes.data_as(_p), M, N, out.ctypes.data_as(_p)))
+    return out
+
+
+def elas_vals_to_canonical(vals_tiled, M: int, N: int):
+    """Canonical kept values [M, N/2] (bf16 bits as uint16 numpy) of a
+    compressed S saved by elas_lowrank_ffn_fwd in the tiled layout
+    ([M, elas_vals_ld(N)] bf16; numpy or torch, copied to the host)."""
+    import numpy as np
+    src = _host_array(vals_tiled, np.uint16, (M, elas_vals_ld(N)), "vals_tiled")
+    out = np.empty((M, N // 2), dtype=np.uint16)
+    _check(lib().elas_vals_to_canonical(src.ctypes.data_as(_p), M, N, out.ctypes.data_as(_p)))
+    return out
+
+
+def elas_debug_sync(enable: bool | None = None) -> bool:
+    """Switch the ELAS_DEBUG_SYNC mode (synchronise after every kernel and
+    report failures by kernel) on or off; None leaves it.  Returns the
+    previous state."""
+    return bool(lib().elas_debug_sync(-1 if enable is None else (1 if enable else 0)))
 
 
 def elas_timing_enable(enable: bool = True) -> None:

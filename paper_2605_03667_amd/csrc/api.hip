@@ -38,9 +38,16 @@ int check_ptr(const void* p, const char* name) {
     if (rc_ != ELAS_OK) return rc_; \
   } while (0)
 
+// Status of a launch sequence: its own error, else (ELAS_DEBUG_SYNC) the
+// first failure seen when synchronising after one of its kernels.
 int device_status(hipError_t e, const char* what) {
-  if (e == hipSuccess) return ELAS_OK;
-  return fail(ELAS_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+  if (e != hipSuccess) return fail(ELAS_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+  const char* tag = nullptr;
+  const hipError_t d = elas::debug_sync_error(&tag);
+  if (d != hipSuccess)
+    return fail(ELAS_ERR_DEVICE, "%s: kernel %s failed (ELAS_DEBUG_SYNC): %s", what, tag ? tag : "?",
+                hipGetErrorString(d));
+  return ELAS_OK;
 }
 
 // Sizes are bounded so every element offset fits comfortably in int64 and in
@@ -58,6 +65,23 @@ int check_ffn_dims(int64_t T, int64_t d, int64_t d_ff, int64_t r) {
   return ELAS_OK;
 }
 
+// Host-side conversion of the tiled compressed layout (the FFN's saved S) to
+// the canonical one: entry j of row i sits at tiled element
+// (i / 256) * 256 * ld + (j / BW) * R * BW + (i % 256) * BW + j % BW,
+// R = the rows of i's block of 256.
+template <class E, int BW>
+int tiled_to_canonical(const E* tiled, int64_t M, int64_t ld, int64_t n_out, E* out, const char* what) {
+  g_last_error.clear();
+  if (M < 0 || M > kMaxDim) return fail(ELAS_ERR_SHAPE, "M=%lld out of range", (long long)M);
+  if (M == 0) return ELAS_OK;
+  if (tiled == nullptr || out == nullptr) return fail(ELAS_ERR_NULL, "%s: NULL buffer", what);
+  for (int64_t i = 0; i < M; ++i) {
+    const int64_t b = i / 256, R = M - b * 256 < 256 ? M - b * 256 : 256;
+    const E* blk = tiled + b * 256 * ld;
+    for (int64_t j = 0; j < n_out; ++j) out[i * n_out + j] = blk[(j / BW) * R * BW + (i % 256) * BW + j % BW];
+  }
+  return ELAS_OK;
+}
 }  // namespace
 
 extern "C" {
@@ -83,6 +107,7 @@ int64_t elas_meta_ld(int64_t N) { return N > 0 ? elas::meta_ld(N) : 0; }
 int elas_sparsify_24(const uint16_t* h, int64_t M, int64_t N, uint32_t flags, uint16_t* vals,
                      uint8_t* meta, void* stream) {
   g_last_error.clear();
+  elas::debug_sync_reset();
   if (flags & ~ELAS_SPARSIFY_RAW) return fail(ELAS_ERR_FLAGS, "unknown flags 0x%x", flags);
   if (M < 0 || M > kMaxDim) return fail(ELAS_ERR_SHAPE, "M=%lld out of range", (long long)M);
   if (N <= 0 || N % 8 || N > kMaxDim)
@@ -108,6 +133,7 @@ int elas_spmm_24(const uint16_t* a_vals, const uint8_t* a_meta, int64_t M, int64
                  int64_t N, int b_layout, uint16_t* c, void* workspace, size_t workspace_bytes,
                  void* stream) {
   g_last_error.clear();
+  elas::debug_sync_reset();
   if (b_layout != ELAS_B_KN && b_layout != ELAS_B_NK)
     return fail(ELAS_ERR_FLAGS, "b_layout must be ELAS_B_KN or ELAS_B_NK");
   if (M < 0 || M > kMaxDim) return fail(ELAS_ERR_SHAPE, "M=%lld out of range", (long long)M);
@@ -139,6 +165,7 @@ int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t
                          uint16_t* y, uint16_t* P, uint16_t* s_vals, uint8_t* s_meta, uint16_t* Z,
                          void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
+  elas::debug_sync_reset();
   if (flags & ~(ELAS_MODE_DENSE | ELAS_FACTORS_AB | ELAS_FWD_FUSED | ELAS_FWD_UNFUSED))
     return fail(ELAS_ERR_FLAGS,
                 "forward flags: only ELAS_MODE_DENSE, ELAS_FACTORS_AB, ELAS_FWD_FUSED and ELAS_FWD_UNFUSED are allowed");
@@ -187,6 +214,7 @@ int elas_lowrank_ffn_bwd(const uint16_t* dy, const uint16_t* x, const uint16_t* 
                          const uint8_t* s_meta, const uint16_t* Z, uint16_t* dx, float* dU_up, float* dV_up,
                          float* dU_down, float* dV_down, void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
+  elas::debug_sync_reset();
   if (flags & ~(ELAS_MODE_DENSE | ELAS_BWD_STE))
     return fail(ELAS_ERR_FLAGS, "backward flags: only ELAS_MODE_DENSE or ELAS_BWD_STE are allowed");
   const bool dense = (flags & ELAS_MODE_DENSE) != 0, ste = (flags & ELAS_BWD_STE) != 0;
@@ -228,6 +256,7 @@ int elas_lowrank_ffn_bwd(const uint16_t* dy, const uint16_t* x, const uint16_t* 
 int elas_fullrank_ffn_fwd(const uint16_t* x, const uint16_t* W_up, const uint16_t* W_down, int64_t T, int64_t d,
                           int64_t d_ff, uint16_t* y, uint16_t* S, void* stream) {
   g_last_error.clear();
+  elas::debug_sync_reset();
   ELAS_CHECK(check_ffn_dims(T, d, d_ff, 8));
   if (T == 0) return ELAS_OK;
   ELAS_CHECK(check_ptr(x, "x"));
@@ -237,6 +266,23 @@ int elas_fullrank_ffn_fwd(const uint16_t* x, const uint16_t* W_up, const uint16_
   ELAS_CHECK(check_ptr(S, "S"));
   return device_status(elas::run_fullrank_fwd(x, W_up, W_down, T, d, d_ff, y, S, (hipStream_t)stream),
                        "full-rank forward launch");
+}
+
+
+int elas_meta_to_canonical(const uint8_t* meta_tiled, int64_t M, int64_t N, uint8_t* meta_canonical) {
+  if (N <= 0 || N % 8 || N > 65536) {
+    g_last_error.clear();
+    return fail(ELAS_ERR_SHAPE, "N=%lld must be a positive multiple of 8, at most 65536", (long long)N);
+  }
+  return tiled_to_canonical<uint8_t, 8>(meta_tiled, M, elas::meta_ld(N), N / 8, meta_canonical, "meta");
+}
+
+int elas_vals_to_canonical(const uint16_t* vals_tiled, int64_t M, int64_t N, uint16_t* vals_canonical) {
+  if (N <= 0 || N % 8 || N > 65536) {
+    g_last_error.clear();
+    return fail(ELAS_ERR_SHAPE, "N=%lld must be a positive multiple of 8, at most 65536", (long long)N);
+  }
+  return tiled_to_canonical<uint16_t, 32>(vals_tiled, M, elas::vals_ld(N), N / 2, vals_canonical, "vals");
 }
 
 }  // extern "C"

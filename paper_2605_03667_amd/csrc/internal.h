@@ -13,8 +13,12 @@ inline int64_t vals_ld(int64_t n) { return 32 * ((n + 63) / 64); }
 inline int64_t meta_ld(int64_t n) { return 8 * ((n + 63) / 64); }
 inline int64_t pad64(int64_t n) { return 64 * ((n + 63) / 64); }
 
-// timing.hip: brackets one launch with events when timing is enabled
+// timing.hip: brackets one launch with events when timing is enabled, and
+// synchronises after it in the ELAS_DEBUG_SYNC mode (the first failure of
+// the calling thread is kept with its kernel tag until the next reset)
 bool timing_enabled();
+void debug_sync_reset();
+hipError_t debug_sync_error(const char** tag);
 class TimedLaunch {
  public:
   TimedLaunch(const char* tag, hipStream_t stream);

@@ -1,6 +1,7 @@
 // Per-kernel timing for benchmarking: while enabled, every launch made by an
 // entry point is bracketed by two hipEvents recorded on the launch stream.
 // Events are created once and reused; nothing is allocated on the device.
+#include <stdlib.h>
 #include <string.h>
 
 #include <string>
@@ -40,9 +41,29 @@ hipEvent_t next_event() {
   return g_pool[g_next++];
 }
 
+// ELAS_DEBUG_SYNC: initial state from the environment variable of that name
+// (set and not "0"), then whatever elas_debug_sync() last set.
+int debug_sync_initial() {
+  const char* v = getenv("ELAS_DEBUG_SYNC");
+  return v != nullptr && v[0] != '\0' && strcmp(v, "0") != 0;
+}
+int g_debug_sync = debug_sync_initial();
+thread_local hipError_t g_debug_error = hipSuccess;
+thread_local const char* g_debug_tag = nullptr;
+
 }  // namespace
 
 bool timing_enabled() { return g_enabled; }
+
+void debug_sync_reset() {
+  g_debug_error = hipSuccess;
+  g_debug_tag = nullptr;
+}
+
+hipError_t debug_sync_error(const char** tag) {
+  if (tag) *tag = g_debug_tag;
+  return g_debug_error;
+}
 
 TimedLaunch::TimedLaunch(const char* tag, hipStream_t stream) : tag_(tag), stream_(stream) {
   if (!g_enabled || (!g_only.empty() && g_only != tag)) return;
@@ -52,9 +73,18 @@ TimedLaunch::TimedLaunch(const char* tag, hipStream_t stream) : tag_(tag), strea
 }
 
 TimedLaunch::~TimedLaunch() {
-  if (!g_enabled || !start_ || !stop_) return;
-  hipEventRecord(stop_, stream_);
-  g_records.push_back({tag_, start_, stop_});
+  if (g_enabled && start_ && stop_) {
+    hipEventRecord(stop_, stream_);
+    g_records.push_back({tag_, start_, stop_});
+  }
+  if (g_debug_sync) {
+    // wait for this launch and keep the first failure with its kernel tag
+    const hipError_t e = hipStreamSynchronize(stream_);
+    if (e != hipSuccess && g_debug_error == hipSuccess) {
+      g_debug_error = e;
+      g_debug_tag = tag_;
+    }
+  }
 }
 
 }  // namespace elas
@@ -69,6 +99,12 @@ int elas_timing_enable(int enable) {
     elas::g_next = 0;
   }
   return ELAS_OK;
+}
+
+int elas_debug_sync(int enable) {
+  const int prev = elas::g_debug_sync;
+  if (enable >= 0) elas::g_debug_sync = enable != 0;
+  return prev;
 }
 
 int elas_timing_only(const char* tag) {

@@ -32,7 +32,7 @@ def _defines():
 
 def test_exports_every_declared_symbol():
     names = _declared()
-    assert len(names) == 16, names
+    assert len(names) == 19, names
     lib = ctypes.CDLL(elas.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -191,3 +191,82 @@ def test_timing_filter_is_host_only():
     assert L.elas_timing_only(None) == 0
     assert L.elas_timing_only(b"") == 0
 
+
+
+def _cpu(shape, dtype=None):
+    import torch
+    return torch.zeros(shape, dtype=dtype or torch.bfloat16)
+
+
+def test_binding_rejects_mismatched_shapes():
+    """The binding checks every tensor's shape against the sizes it passes to
+    the C ABI (which cannot check buffer sizes) before taking any pointer,
+    so a wrong size raises instead of reading or writing out of bounds.
+    Nothing is launched: the tensors are on the CPU."""
+    import torch
+    T, d, F, r = 8, 16, 24, 8
+    ldv, ldm = elas.elas_vals_ld(F), elas.elas_meta_ld(F)
+    x, dy = _cpu((T, d)), _cpu((T, d))
+    fac = {"U_up": _cpu((d, r)), "V_up": _cpu((r, F)), "U_down": _cpu((F, r)), "V_down": _cpu((r, d))}
+    sparse_saved = {"y": _cpu((T, d)), "P": _cpu((T, r)), "s_vals": _cpu((T, ldv)),
+                    "s_meta": _cpu((T, ldm), torch.uint8), "Z": _cpu((T, r))}
+    dense_saved = dict(sparse_saved, s_vals=_cpu((T, F)), s_meta=None)
+    f32 = torch.float32
+    grads = {"dx": _cpu((T, d)), "dU_up": _cpu((d, r), f32), "dV_up": _cpu((r, F), f32),
+             "dU_down": _cpu((F, r), f32), "dV_down": _cpu((r, d), f32)}
+
+    def raises(match, fn, *a, **k):
+        with pytest.raises(ValueError, match=match):
+            fn(*a, **k)
+
+    bwd = elas.elas_lowrank_ffn_bwd
+    # a sparse forward's saved tensors with the dense flag (s_vals half as wide), and vice versa
+    raises("s_vals \\(dense mode\\)", bwd, dy, x, *fac.values(), sparse_saved, flags=elas.ELAS_MODE_DENSE, grads=grads)
+    raises("s_vals \\(2:4 mode\\)", bwd, dy, x, *fac.values(), dense_saved, flags=0, grads=grads)
+    raises("s_meta", bwd, dy, x, *fac.values(), dict(sparse_saved, s_meta=_cpu((T, ldm - 8), torch.uint8)), grads=grads)
+    for k in grads:
+        bad = dict(grads, **{k: _cpu((grads[k].shape[0] + 1, grads[k].shape[1]), grads[k].dtype)})
+        raises(k, bwd, dy, x, *fac.values(), sparse_saved, grads=bad)
+    raises("dy", bwd, _cpu((T + 1, d)), x, *fac.values(), sparse_saved, grads=grads)
+    raises("U_down", bwd, dy, x, fac["U_up"], fac["V_up"], _cpu((F + 8, r)), fac["V_down"], sparse_saved, grads=grads)
+    fwd = elas.elas_lowrank_ffn_fwd
+    raises("V_down", fwd, x, fac["U_up"], fac["V_up"], fac["U_down"], _cpu((r, d + 8)), out=sparse_saved)
+    raises("Z", fwd, x, *fac.values(), out=dict(sparse_saved, Z=_cpu((T, r + 8))))
+    raises("s_vals \\(dense mode\\)", fwd, x, *fac.values(), flags=elas.ELAS_MODE_DENSE, out=sparse_saved)
+    # factors given as A, B (transposed) without the flag
+    raises("U_up", fwd, x, *(t.t().contiguous() for t in fac.values()), out=sparse_saved)
+    # standalone calls
+    raises("vals", elas.elas_sparsify_24, _cpu((T, F)), vals=_cpu((T, ldv - 8)), meta=_cpu((T, ldm), torch.uint8))
+    raises("a_vals", elas.elas_spmm_24, _cpu((T, F // 2)), _cpu((T, ldm), torch.uint8), F, _cpu((r, F)), elas.ELAS_B_NK)
+    raises("b", elas.elas_spmm_24, _cpu((T, ldv)), _cpu((T, ldm), torch.uint8), F, _cpu((r, F)), elas.ELAS_B_KN)
+    raises("c", elas.elas_spmm_24, _cpu((T, ldv)), _cpu((T, ldm), torch.uint8), F, _cpu((r, F)), elas.ELAS_B_NK,
+           c=_cpu((T, r + 8)))
+    raises("W_down", elas.elas_fullrank_ffn_fwd, x, _cpu((F, d)), _cpu((F, d)))
+
+
+def test_canonical_converters_match_the_tiled_formula():
+    """elas_meta_to_canonical / elas_vals_to_canonical undo the tiled layout
+    of include/elas.h: checked against the independent test formula
+    (tests/helpers.untile) on random contents, with a ragged last row block,
+    and padding columns dropped."""
+    from tests.helpers import tile
+    g = np.random.default_rng(3)
+    for M, N in [(1, 8), (255, 64), (600, 5464), (513, 200)]:
+        ldv, ldm = elas.elas_vals_ld(N), elas.elas_meta_ld(N)
+        rows_v = g.integers(0, 1 << 16, (M, ldv), dtype=np.uint16)
+        rows_m = g.integers(0, 256, (M, ldm), dtype=np.uint8)
+        tv, tm = tile(rows_v, 32).reshape(M, ldv), tile(rows_m, 8).reshape(M, ldm)
+        np.testing.assert_array_equal(elas.elas_vals_to_canonical(tv, M, N), rows_v[:, : N // 2])
+        np.testing.assert_array_equal(elas.elas_meta_to_canonical(tm, M, N), rows_m[:, : N // 8])
+    L = elas.lib()
+    assert L.elas_meta_to_canonical(None, 0, 64, None) == 0
+    assert L.elas_meta_to_canonical(None, 4, 64, None) == elas._STATUS_CODE["ELAS_ERR_NULL"]
+    assert L.elas_vals_to_canonical(FAKE, 4, 12, FAKE) == elas._STATUS_CODE["ELAS_ERR_SHAPE"]
+
+
+def test_debug_sync_switch():
+    prev = elas.elas_debug_sync(None)
+    assert elas.elas_debug_sync(True) == prev
+    assert elas.elas_debug_sync(None) is True
+    assert elas.elas_debug_sync(False) is True
+    assert elas.elas_debug_sync(prev) is False
