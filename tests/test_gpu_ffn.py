@@ -154,6 +154,15 @@ def assert_bit_exact(gpu, f, b, F):
         np.testing.assert_array_equal(gpu[k], b[k], err_msg=k)
 
 
+def sparse_sign_inputs(T, d, F, r, density, scale_log2, seed):
+    """x, U_up, V_up, U_down, V_down, dY as sparse +-2**scale (densities and
+    scales in that order): small exact values for the bit-exact tests."""
+    names = ["x", "U_up", "V_up", "U_down", "V_down", "dY"]
+    shapes = [(T, d), (d, r), (r, F), (F, r), (r, d), (T, d)]
+    return {n: sparse_sign_bf16(shp, de, seed + i, sc)
+            for i, (n, shp, de, sc) in enumerate(zip(names, shapes, density, scale_log2))}
+
+
 def exact_int_inputs(T, d, F, r):
     return {
         "x": uniform_int_bf16((T, d), -1, 1, 1), "U_up": uniform_int_bf16((d, r), -1, 1, 2),
@@ -203,10 +212,7 @@ def test_exact_1b_shape_every_token():
     and split-K (b2, b7) over every token, and every output, including the
     four fp32 weight gradients, must match the oracle bit for bit."""
     T, d, F, r = 4096, 2048, 5464, 512
-    names = ["x", "U_up", "V_up", "U_down", "V_down", "dY"]
-    shapes = [(T, d), (d, r), (r, F), (F, r), (r, d), (T, d)]
-    dens, scale = [1 / 16, 1 / 16, 1 / 64, 1 / 8, 1 / 8, 1 / 4], [0, 0, 0, -8, -4, 0]
-    bits = {n: sparse_sign_bf16(shp, de, 51 + i, sc) for i, (n, shp, de, sc) in enumerate(zip(names, shapes, dens, scale))}
+    bits = sparse_sign_inputs(T, d, F, r, [1 / 16, 1 / 16, 1 / 64, 1 / 8, 1 / 8, 1 / 4], [0, 0, 0, -8, -4, 0], 51)
     bits["V_up"][:, 5461:] = 0
     bits["U_down"][5461:, :] = 0
     f, b = offn.run(bits)
@@ -483,7 +489,7 @@ def test_fused_forward_exact(T):
     every output of the fused forward and of the backward on its saved
     tensors equals the oracle's bit for bit."""
     d, F, r = 64, 1000, 128
-    bits = exact_int_inputs(T, d, F, r)
+    bits = sparse_sign_inputs(T, d, F, r, [1 / 8, 1 / 4, 1 / 4, 1 / 4, 1 / 4, 1 / 16], [0, 0, 0, -8, -4, 0], 61)
     f, b = offn.run(bits)
     assert all_sums_exact(bits, f, b)
     gpu = run_gpu(bits, fwd_flags=elas.ELAS_FWD_FUSED)
