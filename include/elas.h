@@ -198,6 +198,33 @@ int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t
                          uint16_t* Z, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * elas_lowrank_ffn_fwd_noalloc -- for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): elas_lowrank_ffn_fwd with the same arguments, flags,
+ * outputs and results (bit for bit), but without a workspace argument.  Its
+ * workspace is a static device array of ELAS_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every device it runs on until the process ends; the call
+ * itself allocates nothing (no hipMalloc, no allocating library routine).
+ * The first call on a device looks the array's address up there.
+ * Errors: as elas_lowrank_ffn_fwd, plus ELAS_ERR_WORKSPACE when the shape
+ * needs more workspace than the array holds
+ * (elas_lowrank_ffn_fwd_workspace_bytes > ELAS_NOALLOC_SCRATCH_BYTES; at the
+ * largest model shape, d = 2048, d_ff = 5464, r = 512, it needs about 31 MB
+ * at any token count), and ELAS_ERR_DEVICE if the address lookup fails.
+ * Each call overwrites every part of the array it reads (nothing needs to
+ * start at zero).  All calls on one device share the array: calls that
+ * overlap in time on one device (different streams or threads) race and must
+ * be ordered by the caller.
+ */
+#define ELAS_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+size_t elas_noalloc_scratch_bytes(void);
+int elas_lowrank_ffn_fwd_noalloc(const uint16_t* x, const uint16_t* U_up, const uint16_t* V_up,
+                                 const uint16_t* U_down, const uint16_t* V_down,
+                                 int64_t T, int64_t d, int64_t d_ff, int64_t r, uint32_t flags,
+                                 uint16_t* y, uint16_t* P, uint16_t* s_vals, uint8_t* s_meta,
+                                 uint16_t* Z, void* stream);
+
+/*
  * elas_lowrank_ffn_bwd -- backward of the block (Sec. 3.3.2, Sec. 3.4).
  *
  * dy [T,d] bf16 is dL/dY; x, U_up, V_up, U_down, V_down as in the forward;

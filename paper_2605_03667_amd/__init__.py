@@ -22,7 +22,7 @@ __all__ = [
     "elas_spmm_24_workspace_bytes", "elas_lowrank_ffn_fwd", "elas_lowrank_ffn_fwd_workspace_bytes",
     "elas_lowrank_ffn_bwd", "elas_lowrank_ffn_bwd_workspace_bytes", "elas_fullrank_ffn_fwd",
     "elas_timing_enable", "elas_timing_only", "elas_timing_collect", "elas_meta_to_canonical",
-    "elas_vals_to_canonical", "elas_debug_sync",
+    "elas_vals_to_canonical", "elas_debug_sync", "elas_lowrank_ffn_fwd_noalloc", "elas_noalloc_scratch_bytes",
     "ELAS_SPARSIFY_RELU2", "ELAS_SPARSIFY_RAW", "ELAS_B_KN", "ELAS_B_NK", "ELAS_MODE_SPARSE24",
     "ELAS_MODE_DENSE", "ELAS_BWD_STE", "ELAS_FACTORS_AB", "ELAS_FWD_FUSED", "ELAS_FWD_UNFUSED",
 ]
@@ -70,6 +70,8 @@ _SIGNATURES = {
     "elas_spmm_24": ([_p, _p, _i64, _i64, _p, _i64, ctypes.c_int, _p, _p, _sz, _p], ctypes.c_int),
     "elas_lowrank_ffn_fwd_workspace_bytes": ([_i64, _i64, _i64, _i64, _u32], _sz),
     "elas_lowrank_ffn_fwd": ([_p] * 5 + [_i64] * 4 + [_u32] + [_p] * 5 + [_p, _sz, _p], ctypes.c_int),
+    "elas_noalloc_scratch_bytes": ([], _sz),
+    "elas_lowrank_ffn_fwd_noalloc": ([_p] * 5 + [_i64] * 4 + [_u32] + [_p] * 5 + [_p], ctypes.c_int),
     "elas_lowrank_ffn_bwd_workspace_bytes": ([_i64, _i64, _i64, _i64, _u32], _sz),
     "elas_lowrank_ffn_bwd": ([_p] * 6 + [_i64] * 4 + [_u32] + [_p] * 4 + [_p] * 5 + [_p, _sz, _p],
                              ctypes.c_int),
@@ -252,6 +254,42 @@ def elas_lowrank_ffn_fwd(x, U_up, V_up, U_down, V_down, flags: int = 0, out: dic
         _ptr(out["s_meta"], torch.uint8, "s_meta"), _ptr(out["Z"], bf, "Z"),
         _ptr(workspace, torch.uint8, "workspace"), 0 if workspace is None else workspace.numel(),
         _stream(dev)))
+    return out
+
+
+def elas_noalloc_scratch_bytes() -> int:
+    return lib().elas_noalloc_scratch_bytes()
+
+
+def elas_lowrank_ffn_fwd_noalloc(x, U_up, V_up, U_down, V_down, flags: int = 0, out: dict | None = None) -> dict:
+    """elas_lowrank_ffn_fwd without a workspace: the library's static device
+    scratch is used instead, and nothing is allocated by the call (the output
+    tensors must be passed in ``out`` for that; when ``out`` is None they are
+    allocated here, by torch, before the call).  Returns the outputs dict."""
+    T, d = x.shape
+    ab = bool(flags & ELAS_FACTORS_AB)
+    r = U_up.shape[0] if ab else U_up.shape[1]
+    F = V_up.shape[0] if ab else V_up.shape[1]
+    dev = x.device
+    dense = bool(flags & ELAS_MODE_DENSE)
+    for t, shp, name in ((U_up, (d, r), "U_up"), (V_up, (r, F), "V_up"), (U_down, (F, r), "U_down"),
+                         (V_down, (r, d), "V_down")):
+        _shape(t, shp[::-1] if ab else shp, name)
+    if out is None:
+        out = {
+            "y": torch.empty((T, d), dtype=torch.bfloat16, device=dev),
+            "P": torch.empty((T, r), dtype=torch.bfloat16, device=dev),
+            "s_vals": torch.empty((T, F if dense else elas_vals_ld(F)), dtype=torch.bfloat16, device=dev),
+            "s_meta": None if dense else torch.empty((T, elas_meta_ld(F)), dtype=torch.uint8, device=dev),
+            "Z": torch.empty((T, r), dtype=torch.bfloat16, device=dev),
+        }
+    _saved_shapes(out, T, d, F, r, dense, with_y=True)
+    bf = torch.bfloat16
+    _check(lib().elas_lowrank_ffn_fwd_noalloc(
+        _ptr(x, bf, "x"), _ptr(U_up, bf, "U_up"), _ptr(V_up, bf, "V_up"), _ptr(U_down, bf, "U_down"),
+        _ptr(V_down, bf, "V_down"), T, d, F, r, flags,
+        _ptr(out["y"], bf, "y"), _ptr(out["P"], bf, "P"), _ptr(out["s_vals"], bf, "s_vals"),
+        _ptr(out["s_meta"], torch.uint8, "s_meta"), _ptr(out["Z"], bf, "Z"), _stream(dev)))
     return out
 
 

@@ -4,6 +4,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <mutex>
 #include <string>
 
 #include "../../include/elas.h"
@@ -82,6 +83,70 @@ int tiled_to_canonical(const E* tiled, int64_t M, int64_t ld, int64_t n_out, E* 
   }
   return ELAS_OK;
 }
+// Checks of the forward's arguments shared by its two entry points; fills
+// the launch arguments (without workspace).  noop: T == 0, nothing to do.
+int prepare_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t* V_up, const uint16_t* U_down,
+                const uint16_t* V_down, int64_t T, int64_t d, int64_t d_ff, int64_t r, uint32_t flags, uint16_t* y,
+                uint16_t* P, uint16_t* s_vals, uint8_t* s_meta, uint16_t* Z, elas::FfnArgs& a, bool& noop) {
+  if (flags & ~(ELAS_MODE_DENSE | ELAS_FACTORS_AB | ELAS_FWD_FUSED | ELAS_FWD_UNFUSED))
+    return fail(ELAS_ERR_FLAGS,
+                "forward flags: only ELAS_MODE_DENSE, ELAS_FACTORS_AB, ELAS_FWD_FUSED and ELAS_FWD_UNFUSED are allowed");
+  const bool dense = (flags & ELAS_MODE_DENSE) != 0, ab = (flags & ELAS_FACTORS_AB) != 0;
+  const bool fused = (flags & ELAS_FWD_FUSED) != 0, unfused = (flags & ELAS_FWD_UNFUSED) != 0;
+  if (fused && unfused) return fail(ELAS_ERR_FLAGS, "ELAS_FWD_FUSED and ELAS_FWD_UNFUSED exclude each other");
+  if (fused && dense) return fail(ELAS_ERR_FLAGS, "ELAS_FWD_FUSED applies to the sparse forward only");
+  ELAS_CHECK(check_ffn_dims(T, d, d_ff, r));
+  if (fused && !elas::fused_fwd_supported(d, r))
+    return fail(ELAS_ERR_SHAPE, "ELAS_FWD_FUSED needs d a multiple of 64 up to 1024 and r = 128 or 256 (d=%lld r=%lld)",
+                (long long)d, (long long)r);
+  noop = T == 0;
+  if (noop) return ELAS_OK;
+  ELAS_CHECK(check_ptr(x, "x"));
+  ELAS_CHECK(check_ptr(U_up, "U_up"));
+  ELAS_CHECK(check_ptr(V_up, "V_up"));
+  ELAS_CHECK(check_ptr(U_down, "U_down"));
+  ELAS_CHECK(check_ptr(V_down, "V_down"));
+  ELAS_CHECK(check_ptr(y, "y"));
+  ELAS_CHECK(check_ptr(P, "P"));
+  ELAS_CHECK(check_ptr(s_vals, "s_vals"));
+  if (!dense) ELAS_CHECK(check_ptr(s_meta, "s_meta"));
+  ELAS_CHECK(check_ptr(Z, "Z"));
+  a.T = T; a.d = d; a.F = d_ff; a.r = r;
+  a.x = x; a.U_up = U_up; a.V_up = V_up; a.U_down = U_down; a.V_down = V_down;
+  a.y = y; a.P = P; a.P_in = P; a.s_vals = s_vals; a.s_meta = s_meta; a.Z = Z;
+  a.dense = dense;
+  a.ab = ab;
+  a.fused = fused ? 1 : unfused ? 2 : 0;
+  return ELAS_OK;
+}
+
+// Workspace of elas_lowrank_ffn_fwd_noalloc: one static array per device,
+// held until the process ends.  Its device address is looked up once per
+// device (with that device current) and kept; the array's name is only a
+// host-side stand-in and is never passed to a kernel.
+constexpr size_t kScratchBytes = ELAS_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+int scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(ELAS_ERR_DEVICE, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(ELAS_ERR_DEVICE, "device %d beyond the supported %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(ELAS_ERR_DEVICE, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return ELAS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -166,41 +231,38 @@ int elas_lowrank_ffn_fwd(const uint16_t* x, const uint16_t* U_up, const uint16_t
                          void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
   elas::debug_sync_reset();
-  if (flags & ~(ELAS_MODE_DENSE | ELAS_FACTORS_AB | ELAS_FWD_FUSED | ELAS_FWD_UNFUSED))
-    return fail(ELAS_ERR_FLAGS,
-                "forward flags: only ELAS_MODE_DENSE, ELAS_FACTORS_AB, ELAS_FWD_FUSED and ELAS_FWD_UNFUSED are allowed");
-  const bool dense = (flags & ELAS_MODE_DENSE) != 0, ab = (flags & ELAS_FACTORS_AB) != 0;
-  const bool fused = (flags & ELAS_FWD_FUSED) != 0, unfused = (flags & ELAS_FWD_UNFUSED) != 0;
-  if (fused && unfused) return fail(ELAS_ERR_FLAGS, "ELAS_FWD_FUSED and ELAS_FWD_UNFUSED exclude each other");
-  if (fused && dense) return fail(ELAS_ERR_FLAGS, "ELAS_FWD_FUSED applies to the sparse forward only");
-  ELAS_CHECK(check_ffn_dims(T, d, d_ff, r));
-  if (fused && !elas::fused_fwd_supported(d, r))
-    return fail(ELAS_ERR_SHAPE, "ELAS_FWD_FUSED needs d a multiple of 64 up to 1024 and r = 128 or 256 (d=%lld r=%lld)",
-                (long long)d, (long long)r);
-  if (T == 0) return ELAS_OK;
-  ELAS_CHECK(check_ptr(x, "x"));
-  ELAS_CHECK(check_ptr(U_up, "U_up"));
-  ELAS_CHECK(check_ptr(V_up, "V_up"));
-  ELAS_CHECK(check_ptr(U_down, "U_down"));
-  ELAS_CHECK(check_ptr(V_down, "V_down"));
-  ELAS_CHECK(check_ptr(y, "y"));
-  ELAS_CHECK(check_ptr(P, "P"));
-  ELAS_CHECK(check_ptr(s_vals, "s_vals"));
-  if (!dense) ELAS_CHECK(check_ptr(s_meta, "s_meta"));
-  ELAS_CHECK(check_ptr(Z, "Z"));
-  const size_t need = elas::fwd_workspace_bytes(T, d, d_ff, r, dense, ab);
+  elas::FfnArgs a{};
+  bool noop = false;
+  ELAS_CHECK(prepare_fwd(x, U_up, V_up, U_down, V_down, T, d, d_ff, r, flags, y, P, s_vals, s_meta, Z, a, noop));
+  if (noop) return ELAS_OK;
+  const size_t need = elas::fwd_workspace_bytes(T, d, d_ff, r, a.dense, a.ab);
   if (workspace_bytes < need)
     return fail(ELAS_ERR_WORKSPACE, "workspace %zu bytes, %zu needed", workspace_bytes, need);
   if (need) ELAS_CHECK(check_ptr(workspace, "workspace"));
-  elas::FfnArgs a{};
-  a.T = T; a.d = d; a.F = d_ff; a.r = r;
-  a.x = x; a.U_up = U_up; a.V_up = V_up; a.U_down = U_down; a.V_down = V_down;
-  a.y = y; a.P = P; a.P_in = P; a.s_vals = s_vals; a.s_meta = s_meta; a.Z = Z;
   a.ws = workspace;
-  a.dense = dense;
-  a.ab = ab;
-  a.fused = fused ? 1 : unfused ? 2 : 0;
   return device_status(elas::run_fwd(a, (hipStream_t)stream), "forward launch");
+}
+
+size_t elas_noalloc_scratch_bytes(void) { return kScratchBytes; }
+
+int elas_lowrank_ffn_fwd_noalloc(const uint16_t* x, const uint16_t* U_up, const uint16_t* V_up,
+                                 const uint16_t* U_down, const uint16_t* V_down, int64_t T, int64_t d, int64_t d_ff,
+                                 int64_t r, uint32_t flags, uint16_t* y, uint16_t* P, uint16_t* s_vals,
+                                 uint8_t* s_meta, uint16_t* Z, void* stream) {
+  g_last_error.clear();
+  elas::debug_sync_reset();
+  elas::FfnArgs a{};
+  bool noop = false;
+  ELAS_CHECK(prepare_fwd(x, U_up, V_up, U_down, V_down, T, d, d_ff, r, flags, y, P, s_vals, s_meta, Z, a, noop));
+  if (noop) return ELAS_OK;
+  const size_t need = elas::fwd_workspace_bytes(T, d, d_ff, r, a.dense, a.ab);
+  if (need > kScratchBytes)
+    return fail(ELAS_ERR_WORKSPACE, "this forward needs %zu bytes of workspace; the static scratch holds %zu",
+                need, kScratchBytes);
+  void* ws = nullptr;
+  if (need) ELAS_CHECK(scratch_address(&ws));
+  a.ws = ws;
+  return device_status(elas::run_fwd(a, (hipStream_t)stream), "forward launch (static scratch)");
 }
 
 size_t elas_lowrank_ffn_bwd_workspace_bytes(int64_t T, int64_t d, int64_t d_ff, int64_t r, uint32_t flags) {
