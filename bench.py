@@ -10,16 +10,25 @@ the choice of the dominant kernel), the timed region, in which the library
 records events around the dominant kernel's launches only (tokens/s and that
 kernel's live average duration), and a reference pass without events.
 Besides tokens/s it reports:
-  roofline  -- the kernel with the largest share of the step: algorithmic
-               FLOP per launch / its average launch time in the timed region
-               vs the bf16 MFMA peak;
-  spgemm    -- the 2:4 sparse x dense down projection (v_smfmac);
-  kernels   -- every kernel's launches, average time and rate (per-kernel pass);
+  roofline  -- the kernel with the largest share of the step, under
+               algorithmic accounting: intensity = algorithmic FLOP /
+               algorithmic bytes per launch; bound = the lower of the bf16
+               MFMA peak and intensity x the HBM peak; achieved and peak in
+               that bound's unit, from its average launch time in the timed
+               region;
+  spgemm    -- the 2:4 sparse x dense down projection (v_smfmac) against the
+               sparse bf16 peak (dense-equivalent), and the same for dP;
+  kernels   -- every kernel's launches, average time, rates, bound and
+               roofline fraction (per-kernel pass);
+  cold      -- the step and the sparsify kernel with the caches flushed
+               before every call (a 512 MB write);
+  configs   -- forward + backward tokens/s of the 60M, 130M and 350M shapes;
 and, timed separately, the standalone sparsify kernel on h [65536 x 2736]
 (the 350M-shape activation) against the HBM peak, the 2:4-compressed vs dense
 activation run at T = 262144 (large_batch), the forward-only comparison with
 the full-rank ReLU^2 FFN at the shapes of the paper's Table 3 (table3), plus
-the CPU oracle on a bounded sample of the same workload (cpu_baseline).
+the CPU oracle on a bounded sample of the same workload and on the whole
+60M-shape workload with one thread (cpu_baseline).
 """
 from __future__ import annotations
 
@@ -66,6 +75,48 @@ def executed_flops(tag: str, T: int, d: int, F: int, r: int) -> float | None:
     if tag in ("k3_spmm_down", "b3_dH_masked", "b4_dU_down", "b5_spmm_dP", "b6_dV_up"):
         return 2.0 * T * r * Fp
     return a
+
+
+def algorithmic_bytes(tag: str, T: int, d: int, F: int, r: int) -> float | None:
+    """HBM bytes one launch must move if every operand is read once and every
+    output written once: bf16 tensors 2 B per element, the compressed 2:4
+    activation 1.125 B per feature (kept values plus 2-bit codes, Table 2's
+    storage), its metadata 0.125 B per feature when read with dH's values,
+    fp32 weight gradients 4 B per element."""
+    S = T * F * 1.125                 # compressed S: F/2 bf16 values + F/8 code bytes per token
+    dH = T * F * 1.0                  # compressed dH values (its codes are S's)
+    meta = T * F * 0.125
+    table = {
+        "k1_up_gemm": 2 * (T * d + d * r + T * r), "k2_up_relu2_sparsify": 2 * (T * r + r * F) + S,
+        "k3_spmm_down": S + 2 * (F * r + T * r), "k4_down_gemm": 2 * (T * r + r * d + T * d),
+        "b1_dZ": 2 * (T * d + r * d + T * r), "b2_dV_down": 2 * (T * r + T * d) + 4 * r * d,
+        "b3_dH_masked": 2 * (T * r + F * r) + S + dH, "b4_dU_down": S + 2 * T * r + 4 * F * r,
+        "b5_spmm_dP": dH + meta + 2 * (r * F + T * r), "b6_dV_up": dH + meta + 2 * T * r + 4 * r * F,
+        "b7_dU_up": 2 * (T * d + T * r) + 4 * d * r, "b8_dx": 2 * (T * r + d * r + T * d),
+    }
+    v = table.get(tag)
+    return None if v is None else float(v)
+
+
+def roofline_of(tag: str, T: int, d: int, F: int, r: int, avg_s: float) -> dict | None:
+    """Roofline of one launch under algorithmic accounting: intensity =
+    algorithmic FLOP / algorithmic bytes; the attainable rate is the lower of
+    the MFMA peak (2.5 PFLOP/s bf16; also the useful-FLOP peak of the 2:4
+    smfmac, which does twice the dense-equivalent work at the dense rate) and
+    intensity x 8 TB/s.  The bound is whichever is lower; achieved and peak
+    are reported in that bound's unit (TFLOP/s or GB/s)."""
+    fl, by = algorithmic_flops(tag, T, d, F, r), algorithmic_bytes(tag, T, d, F, r)
+    if fl is None or by is None:
+        return None
+    ai = fl / by
+    hbm_limited = ai * PEAK_HBM_GBS * 1e9 < PEAK_BF16_TFLOPS * 1e12
+    if hbm_limited:
+        achieved, peak, unit = by / avg_s / 1e9, PEAK_HBM_GBS, "GB/s"
+    else:
+        achieved, peak, unit = fl / avg_s / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
+    return {"bound": "hbm" if hbm_limited else "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 4), "intensity_flop_per_byte": round(ai, 1),
+            "alg_flop_per_launch": fl, "alg_bytes_per_launch": by}
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_llama1b_fwd_bwd.txt")
@@ -317,9 +368,22 @@ def table3_compare(iters: int = 20, warmup: int = 3) -> dict:
             "host_bound_runs": len(host_bound), "models": models}
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(cfg: dict, sample_tokens: int) -> dict:
-    import numpy as np
-    from threadpoolctl import threadpool_info
+    """The oracle as it stands on the host cores: forward + backward on a
+    bounded sample of the 1B-shape workload with every BLAS thread, and the
+    whole 60M-shape workload (2048 tokens) on one thread."""
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle import ffn as offn
     from synthetic import config_inputs
@@ -329,10 +393,76 @@ def cpu_baseline(cfg: dict, sample_tokens: int) -> dict:
     offn.run(bits)
     dt = time.perf_counter() - t0
     threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    small = config_inputs("llama60m")
+    with threadpool_limits(limits=1, user_api="blas"):
+        t1 = time.perf_counter()
+        offn.run(small)
+        dt1 = time.perf_counter() - t1
     return {"value": sample_tokens / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "seconds": dt,
+            "seconds": dt, "cpu_model": cpu_model(),
             "sample": f"{sample_tokens} tokens of the 1B-shape FFN workload (d={cfg['d']}, d_ff={cfg['d_ff']}, "
-                      f"r={cfg['r']}), float64 numpy oracle, forward + backward with bf16 rounding points"}
+                      f"r={cfg['r']}), float64 numpy oracle, forward + backward with bf16 rounding points",
+            "llama60m_one_thread": {"tokens_per_s": round(small["x"].shape[0] / dt1, 1), "seconds": round(dt1, 3),
+                                    "tokens": int(small["x"].shape[0]), "threads": 1}}
+
+
+def cold_us(fn, iters: int, flush) -> dict:
+    """Device time of fn per call with the caches cold: before every call a
+    write of `flush` (512 MB, twice the 256 MB Infinity Cache and far more
+    than the L2s) evicts the inputs; each call is bracketed by its own
+    events on the current stream."""
+    import torch
+    out = []
+    for i in range(iters):
+        flush.fill_(i & 0xFF)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        torch.cuda.synchronize()
+        out.append(a.elapsed_time(b) * 1e3)
+    out.sort()
+    return {"median_us": round(out[len(out) // 2], 2), "min_us": round(out[0], 2), "iters": iters}
+
+
+def config_steps(name: str, steps: int, warmup: int) -> dict:
+    """Forward + backward tokens/s of one named workload (warm caches)."""
+    import numpy as np
+    import torch
+
+    import paper_2605_03667_amd as elas
+    from synthetic import CONFIGS, config_inputs
+
+    c = CONFIGS[name]
+    T, d, F, r = c["T"], c["d"], c["d_ff"], c["r"]
+    dev = torch.device("cuda:0")
+    t = {k: torch.from_numpy(v.view(np.int16)).view(torch.bfloat16).to(dev) for k, v in config_inputs(name).items()}
+    ws_f = torch.empty(max(1, elas.elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r)), dtype=torch.uint8, device=dev)
+    ws_b = torch.empty(max(1, elas.elas_lowrank_ffn_bwd_workspace_bytes(T, d, F, r)), dtype=torch.uint8, device=dev)
+    saved = elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], workspace=ws_f)
+    grads = elas.elas_lowrank_ffn_bwd(t["dY"], t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], saved,
+                                      workspace=ws_b)
+
+    def step():
+        elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], out=saved, workspace=ws_f)
+        elas.elas_lowrank_ffn_bwd(t["dY"], t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], saved,
+                                  grads=grads, workspace=ws_b)
+
+    for _ in range(warmup):
+        step()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(steps):
+        step()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    out = {"tokens_per_s": round(T / (ms / 1e3), 1), "ms_per_step": round(ms, 4), "steps": steps,
+           "T": T, "d": d, "d_ff": F, "r": r}
+    del t, ws_f, ws_b, saved, grads
+    torch.cuda.empty_cache()
+    return out
 
 
 def main() -> int:
@@ -345,6 +475,8 @@ def main() -> int:
     ap.add_argument("--no-sparsify", action="store_true", help="skip the standalone sparsify measurement")
     ap.add_argument("--no-large-batch", action="store_true",
                     help="skip the T = 262144 compressed-vs-dense activation comparison")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the forward + backward lines of the 60M, 130M and 350M shapes")
     ap.add_argument("--no-table3", action="store_true",
                     help="skip the forward-only ELAS vs full-rank FFN comparison (Table 3 shapes)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -446,15 +578,16 @@ def main() -> int:
         if a is not None:
             row["alg_tflops"] = round(a / (avg_us * 1e-6) / 1e12, 1)
             row["exec_tflops"] = round(executed_flops(tag, T, d, F, r) / (avg_us * 1e-6) / 1e12, 1)
+            rf = roofline_of(tag, T, d, F, r, avg_us * 1e-6)
+            row.update({"bound": rf["bound"], "frac": rf["frac"], "intensity": rf["intensity_flop_per_byte"]})
         ktab[tag] = row
     dom_avg_s = dom_timed[1] / dom_timed[0] / 1e3
-    dom_alg = algorithmic_flops(dom, T, d, F, r)
-    achieved = dom_alg / dom_avg_s / 1e12
     tr = measured_traffic(dom) if args.workload == "llama1b" else None
-    roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": None if tr is None else tr[0] + tr[1],
-                "alg_flop_per_launch": dom_alg, "avg_us": round(dom_avg_s * 1e6, 2)}
+    roofline = dict({"kernel": dom}, **roofline_of(dom, T, d, F, r, dom_avg_s))
+    roofline.update({"traffic": None if tr is None else tr[0] + tr[1], "avg_us": round(dom_avg_s * 1e6, 2),
+                     "alg_tflops": round(algorithmic_flops(dom, T, d, F, r) / dom_avg_s / 1e12, 1),
+                     "frac_of_bf16_mfma_peak": round(algorithmic_flops(dom, T, d, F, r) / dom_avg_s / 1e12
+                                                     / PEAK_BF16_TFLOPS, 4)})
     if tr is not None:
         roofline["traffic_read_bytes"], roofline["traffic_write_bytes"] = tr
         roofline["traffic_source"] = os.path.relpath(TRAFFIC_FILE, ROOT)
@@ -462,9 +595,19 @@ def main() -> int:
     sp_tag = "k3_spmm_down"
     sp_avg_s = kernels[sp_tag][1] / kernels[sp_tag][0] / 1e3
     sp_alg = algorithmic_flops(sp_tag, T, d, F, r) / sp_avg_s / 1e12
+    # The smfmac products: useful (algorithmic) FLOP T r d_ff; the instruction
+    # does the 2:4 operand's dense-equivalent work, twice that, at the dense
+    # bf16 rate, so its dense-equivalent peak is 5.0 PFLOP/s.
+    sp_b5 = kernels["b5_spmm_dP"][1] / kernels["b5_spmm_dP"][0] / 1e3
     spgemm = {"kernel": sp_tag, "avg_us": round(sp_avg_s * 1e6, 2), "alg_tflops": round(sp_alg, 1),
-              "dense_equiv_tflops": round(2 * sp_alg, 1), "frac_of_dense_bf16_peak": round(sp_alg / PEAK_BF16_TFLOPS, 4),
-              "frac_of_sparse_bf16_peak": round(2 * sp_alg / (2 * PEAK_BF16_TFLOPS), 4)}
+              "dense_equiv_tflops": round(2 * sp_alg, 1),
+              "frac_of_sparse_bf16_peak": round(2 * sp_alg / (2 * PEAK_BF16_TFLOPS), 4),
+              "sparse_bf16_peak_tflops": 2 * PEAK_BF16_TFLOPS,
+              "hbm_gbs": round(algorithmic_bytes(sp_tag, T, d, F, r) / sp_avg_s / 1e9, 1),
+              "roofline": roofline_of(sp_tag, T, d, F, r, sp_avg_s),
+              "b5_spmm_dP": {"avg_us": round(sp_b5 * 1e6, 2),
+                             "frac_of_sparse_bf16_peak": round(algorithmic_flops("b5_spmm_dP", T, d, F, r) / sp_b5
+                                                               / 1e12 / PEAK_BF16_TFLOPS, 4)}}
 
     result = {
         "metric": METRIC, "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1,
@@ -478,10 +621,26 @@ def main() -> int:
         "kernels": ktab,
     }
 
+    # ---- cold caches: the same step with the Infinity Cache and L2 flushed
+    # before every step (a 512 MB write) ----
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    cold = cold_us(step, 5, flush)
+    result["cold"] = {"step": dict(cold, tokens_per_s=round(T / (cold["median_us"] * 1e-6), 1),
+                                   flush_bytes=flush.numel())}
+
+    # ---- the other model shapes, forward + backward (warm) ----
+    if not args.no_configs and args.workload == "llama1b":
+        del out, grads, ws_f, ws_b, t
+        torch.cuda.empty_cache()
+        result["configs"] = {n: config_steps(n, args.steps, args.warmup)
+                             for n in ("llama60m", "llama130m", "llama350m")}
+        t = None
+
     # ---- standalone sparsify on h [65536 x 2736] -----------------------------
     if not args.no_sparsify:
         M, N = SPARSIFY_SHAPE
-        del out, grads, ws_f, ws_b, t
+        if t is not None:
+            del out, grads, ws_f, ws_b, t
         torch.cuda.empty_cache()
         h = to_dev(h_input(M, N, seed=2))
         vals = torch.empty((M, elas.elas_vals_ld(N)), dtype=bf, device=dev)
@@ -511,6 +670,11 @@ def main() -> int:
         torch.cuda.synchronize()
         copy_gbs = 2 * h.numel() * 2 / (c0.elapsed_time(c1) / 20 / 1e3) / 1e9
         del hc
+        sp_cold = cold_us(lambda: elas.elas_sparsify_24(h, vals=vals, meta=meta), 10, flush)
+        sp_cold["gbs"] = round(alg_bytes / (sp_cold["median_us"] * 1e-6) / 1e9, 1)
+        sp_cold["frac"] = round(sp_cold["gbs"] / PEAK_HBM_GBS, 4)
+        result["cold"]["sparsify"] = sp_cold
+        del flush
         result["sparsify"] = {"shape": [M, N], "avg_us": round(avg_s * 1e6, 2), "alg_bytes": alg_bytes,
                               "copy_gbs_same_size": round(copy_gbs, 1),
                               "frac_of_copy": round(gbs / copy_gbs, 4),
