@@ -340,7 +340,7 @@ struct SmallSplit {
 SmallSplit plan_small_split(int64_t M, int64_t N, int64_t K, int bk) {
   const int64_t tiles = cdiv(M, 128) * cdiv(N, 128), cus = device_cus();
   const int64_t steps = cdiv(K, bk);
-  if (tiles * 2 > cus || steps < 16) return {1, K};
+  if (tiles == 0 || tiles * 2 > cus || steps < 16) return {1, K};   // (no rows: nothing to split)
   int64_t s = cus / tiles;
   if (s > steps / 8) s = steps / 8;
   if (s < 2) return {1, K};
