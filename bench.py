@@ -22,7 +22,8 @@ Besides tokens/s it reports:
                roofline fraction (per-kernel pass);
   cold      -- the step and the sparsify kernel with the caches flushed
                before every call (a 512 MB write);
-  configs   -- forward + backward tokens/s of the 60M, 130M and 350M shapes;
+  configs   -- forward + backward tokens/s of the 60M, 130M and 350M shapes,
+               and of the 1B shape with the straight-through backward;
 and, timed separately, the standalone sparsify kernel on h [65536 x 2736]
 (the 350M-shape activation) against the HBM peak, the 2:4-compressed vs dense
 activation run at T = 262144 (large_batch), the forward-only comparison with
@@ -425,8 +426,10 @@ def cold_us(fn, iters: int, flush) -> dict:
     return {"median_us": round(out[len(out) // 2], 2), "min_us": round(out[0], 2), "iters": iters}
 
 
-def config_steps(name: str, steps: int, warmup: int) -> dict:
-    """Forward + backward tokens/s of one named workload (warm caches)."""
+def config_steps(name: str, steps: int, warmup: int, bwd_flags: int = 0) -> dict:
+    """Forward + backward tokens/s of one named workload (warm caches);
+    bwd_flags selects the backward (e.g. ELAS_BWD_STE after the 2:4
+    forward)."""
     import numpy as np
     import torch
 
@@ -438,15 +441,16 @@ def config_steps(name: str, steps: int, warmup: int) -> dict:
     dev = torch.device("cuda:0")
     t = {k: torch.from_numpy(v.view(np.int16)).view(torch.bfloat16).to(dev) for k, v in config_inputs(name).items()}
     ws_f = torch.empty(max(1, elas.elas_lowrank_ffn_fwd_workspace_bytes(T, d, F, r)), dtype=torch.uint8, device=dev)
-    ws_b = torch.empty(max(1, elas.elas_lowrank_ffn_bwd_workspace_bytes(T, d, F, r)), dtype=torch.uint8, device=dev)
+    ws_b = torch.empty(max(1, elas.elas_lowrank_ffn_bwd_workspace_bytes(T, d, F, r, bwd_flags)), dtype=torch.uint8,
+                       device=dev)
     saved = elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], workspace=ws_f)
     grads = elas.elas_lowrank_ffn_bwd(t["dY"], t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], saved,
-                                      workspace=ws_b)
+                                      flags=bwd_flags, workspace=ws_b)
 
     def step():
         elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], out=saved, workspace=ws_f)
         elas.elas_lowrank_ffn_bwd(t["dY"], t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], saved,
-                                  grads=grads, workspace=ws_b)
+                                  flags=bwd_flags, grads=grads, workspace=ws_b)
 
     for _ in range(warmup):
         step()
@@ -634,6 +638,9 @@ def main() -> int:
         torch.cuda.empty_cache()
         result["configs"] = {n: config_steps(n, args.steps, args.warmup)
                              for n in ("llama60m", "llama130m", "llama350m")}
+        # the straight-through backward of Eq. 4 after the 2:4 forward, same workload
+        result["configs"]["llama1b_ste_backward"] = config_steps("llama1b", args.steps, args.warmup,
+                                                                  elas.ELAS_BWD_STE)
         t = None
 
     # ---- standalone sparsify on h [65536 x 2736] -----------------------------
@@ -699,7 +706,7 @@ def main() -> int:
         sq_tflops = 2.0 * n_sq ** 3 / (g0.elapsed_time(g1) / 10 / 1e3) / 1e12
         result["mfma_achievable"] = {"gemm": f"bf16 {n_sq}^3, torch.matmul (hipBLASLt)",
                                      "tflops": round(sq_tflops, 1), "frac_of_peak": round(sq_tflops / PEAK_BF16_TFLOPS, 4),
-                                     "dominant_kernel_frac_of_achievable": round(roofline["achieved"] / sq_tflops, 4)}
+                                     "dominant_kernel_alg_tflops_over_achievable": round(roofline["alg_tflops"] / sq_tflops, 4)}
         del a_sq, b_sq, c_sq
         torch.cuda.empty_cache()
 
