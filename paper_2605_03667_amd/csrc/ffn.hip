@@ -540,13 +540,13 @@ FwdWs fwd_ws(char* p, int64_t T, int64_t d, int64_t F, int64_t r, bool ab) {
 }
 
 struct BwdWs {
-  uint16_t *dZ, *dH, *dP, *R, *V_upT;
+  uint16_t *dZ, *dH, *dP, *V_upT;
   float* part;
   size_t bytes;
 };
 // dH is compressed [T x ldv] in the sparse backward and dense [T x F] in the
 // dense and straight-through ones; the straight-through backward also holds
-// the recomputed dense relu(h) [T x F] and V_up^T.
+// V_up^T (relu(h) is recomputed tile by tile inside the dH kernel).
 BwdWs bwd_ws(char* p, int64_t T, int64_t d, int64_t F, int64_t r, bool dense, bool ste) {
   const int64_t Fp = pad64(F);
   Carver c{p};
@@ -554,10 +554,7 @@ BwdWs bwd_ws(char* p, int64_t T, int64_t d, int64_t F, int64_t r, bool dense, bo
   w.dZ = c.take<uint16_t>(T * r);
   w.dH = c.take<uint16_t>(T * ((dense || ste) ? F : vals_ld(F)));
   w.dP = c.take<uint16_t>(T * r);
-  if (ste) {
-    w.R = c.take<uint16_t>(T * F);
-    w.V_upT = c.take<uint16_t>(Fp * r);
-  }
+  if (ste) w.V_upT = c.take<uint16_t>(Fp * r);
   // split-K partials of the products over tokens (d_ff-wide ones have Fp rows
   // when read compressed, F rows when dense)
   size_t pb = partial_bytes(r, d, T, false);
@@ -724,23 +721,21 @@ hipError_t run_bwd(const FfnArgs& a, hipStream_t st) {
     // dense dH [T x F] = dS * 2 r at every position: r = bf16(sqrt(s)) from the
     // dense S (dense mode), or relu(h) recomputed from P and V_up (straight-
     // through estimator of Eq. 4 after a sparse forward)
-    const uint16_t* act = a.s_vals;
-    int square = 1;
-    if (a.ste) {
-      ELAS_TRY(transpose_pad(a.V_up, r, F, F, w.V_upT, Fp, r, r, st));      // [Fp x r], zero rows >= F
-      GemmArgs h{};
-      h.A = w.V_upT; h.lda = r; h.B = a.P_in; h.ldb = r;
-      h.M = Fp; h.N = T; h.K = r; h.m_valid = Fp; h.ka_valid = r; h.kb_valid = r;
-      h.act = w.R; h.ld_act = F; h.f_valid = F; h.act_square = 0;
-      ELAS_TRY(launch_act<EPI_ACT_DENSE>("b3_relu_h_recompute", h, st));
-      act = w.R;
-      square = 0;
-    }
     GemmArgs g{};
     g.A = a.U_down; g.lda = r; g.B = w.dZ; g.ldb = r;
     g.M = Fp; g.N = T; g.K = r; g.m_valid = F; g.ka_valid = r; g.kb_valid = r;
-    g.act = const_cast<uint16_t*>(act); g.ld_act = F; g.f_valid = F; g.act_square = square; g.dact = w.dH;
-    ELAS_TRY(launch_act<EPI_DH_DENSE>(a.ste ? "b3_dH_ste" : "b3_dH_dense", g, st));
+    g.ld_act = F; g.f_valid = F; g.dact = w.dH;
+    if (a.ste) {
+      // one kernel per tile: h^T = V_up^T P^T over the first r contraction
+      // steps (V_up^T rows >= F read as zero), relu(h) kept in registers, then
+      // dS^T = U_down dZ^T over the next r
+      ELAS_TRY(transpose_pad(a.V_up, r, F, F, w.V_upT, Fp, r, r, st));      // [Fp x r], zero rows >= F
+      g.A = w.V_upT; g.B = a.P_in; g.A2 = a.U_down; g.B2 = w.dZ;
+      ELAS_TRY(launch_act<EPI_DH_STE>("b3_dH_ste", g, st));
+    } else {
+      g.act = const_cast<uint16_t*>(a.s_vals); g.act_square = 1;
+      ELAS_TRY(launch_act<EPI_DH_DENSE>("b3_dH_dense", g, st));
+    }
     if (a.dense) {
       // dU_down = S^T dZ with the dense S
       ELAS_TRY(gemm_tt_f32<OP_T>("b4_dU_down_dense", a.s_vals, F, nullptr, 0, w.dZ, r, F, r, T, w.part, a.dU_down, F,

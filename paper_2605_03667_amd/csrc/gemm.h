@@ -59,6 +59,7 @@ enum EpiMode {
   EPI_DH = 3,         // dH = dS * mask * 2 relu(h), compressed (C = dS^T)
   EPI_ACT_DENSE = 4,  // dense activation: relu(h)^2 (act_square) or relu(h) (C = H^T)
   EPI_DH_DENSE = 5,   // dense dH = dS * 2 r, r from a dense activation (C = dS^T)
+  EPI_DH_STE = 6,     // dense dH = dS * 2 relu(h), h = A B^T of the first operand pair (C = dS^T)
 };
 
 struct GemmArgs {
@@ -68,6 +69,11 @@ struct GemmArgs {
   int64_t ldam;        // byte pitch of the metadata
   const uint16_t* B;   // OP_K [N x K], OP_T [K x N]
   int64_t ldb;
+  // EPI_DH_STE: the second operand pair (same shapes and pitches as A, B).
+  // The tile's contraction runs over (A, B) first, whose product is H^T, then
+  // over (A2, B2), whose product is dS^T.
+  const uint16_t* A2;
+  const uint16_t* B2;
   int64_t M, N, K;     // C is M x N; contraction length K (dense count)
   int64_t m_valid;     // rows of A that exist in memory (rows >= m_valid read as 0)
   int64_t ka_valid;    // contraction entries of A that exist (>= read as 0)
@@ -194,6 +200,7 @@ struct GemmCfg {
   static_assert(DEEP_ == 0 || (STAGES_ == 2 && !STAGED_EPI && DIRECT), "three-stage ring: plain epilogues, direct staging");
   static_assert(!STAGED_EPI || (BM_ == 256 && BN_ * BM_ <= STAGE && DIRECT), "staged epilogue layout");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+  static_assert(EPI_ != EPI_DH_STE || AMODE_ != OP_TSP, "two operand pairs: direct staging");
 };
 
 // LDS chunk swizzle.  Fragment reads touch 8 consecutive rows at one chunk;
@@ -606,6 +613,9 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
   const int64_t kbeg = (int64_t)by * g.k_split;
   const int64_t kend = kbeg + g.k_split < g.K ? kbeg + g.k_split : g.K;
   const int nsteps = kend > kbeg ? (int)((kend - kbeg + BK - 1) / BK) : 0;
+  // EPI_DH_STE: a tile runs its K steps twice, over the two operand pairs
+  constexpr bool TWO = Cfg::EPI == EPI_DH_STE;
+  const int tsteps = TWO ? 2 * nsteps : nsteps;
   const int lrow = lane & 31, lhalf = lane >> 5;
   // Panel of this workgroup's XCD (m_groups > 1): M tiles [pm_begin, +pm_count),
   // N tiles from pn_begin; tiles are then numbered locally, M fastest.
@@ -639,6 +649,21 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       for (int j = 0; j < FN; ++j)
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  };
+  // EPI_DH_STE: relu(h) of the tile (h = the first pair's product), rounded
+  // to bf16 and packed in pairs in the accumulator layout, kept in registers
+  // while the second pair accumulates dS^T.
+  uint32_t hst[TWO ? FM : 1][TWO ? FN : 1][8];
+  auto stash_h = [&]() __attribute__((always_inline)) {
+    if constexpr (TWO) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int q = 0; q < 8; ++q) hst[i][j][q] = bf16x2_rne(relu_f32(acc[i][j][2 * q]), relu_f32(acc[i][j][2 * q + 1]));
+      zero_acc();
+    }
   };
 
   // MFMAs of one K step on the LDS stage at `base`.  Fragments of sub-step
@@ -838,16 +863,20 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             if (inside || (row + dr < g.M && col < g.N)) base[dr * g.ldc] = (__bf16)acc[i][j][e];
           }
         }
-    } else if constexpr (Cfg::EPI == EPI_ACT_DENSE || Cfg::EPI == EPI_DH_DENSE) {
+    } else if constexpr (Cfg::EPI == EPI_ACT_DENSE || Cfg::EPI == EPI_DH_DENSE || Cfg::EPI == EPI_DH_STE) {
       // C rows are features f, columns tokens t: accumulators 4b..4b+3 of a
       // lane are features 8b + 4h + 0..3 of token column l % 32.  Lanes l and
       // l+32 exchange halves so that each writes 16 contiguous features
       // (half 0: 0..15, half 1: 16..31 of the 32-row block) of its token row.
+      // (EPI_DH_STE: the lane index laundered, so that the store offsets are
+      // formed here rather than kept live beside the stashed relu(h).)
+      int lr = lrow, lh = lhalf;
+      if constexpr (Cfg::EPI == EPI_DH_STE) asm volatile("" : "+v"(lr), "+v"(lh));
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-          const int64_t t = n0 + wn * TN + j * 32 + lrow;
+          const int64_t t = n0 + wn * TN + j * 32 + lr;
           const int64_t f32 = m0 + wm * TM + i * 32;
           uint2 mine[4];   // block b: features f32 + 8b + 4h .. +3 as 4 bf16
           if constexpr (Cfg::EPI == EPI_ACT_DENSE) {
@@ -867,12 +896,26 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
               }
               mine[b] = make_uint2(v[0], v[1]);
             }
+          } else if constexpr (Cfg::EPI == EPI_DH_STE) {
+            // relu(h) from the stash: accumulator 4b + q of the h product is
+            // feature 8b + 4h + q, as for dS
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+              uint32_t v[2];
+#pragma unroll
+              for (int e = 0; e < 2; ++e) {
+                const uint32_t rr = hst[i][j][2 * b + e];
+                v[e] = bf16x2_rne(acc[i][j][4 * b + 2 * e] * 2.0f * __builtin_bit_cast(float, rr << 16),
+                                  acc[i][j][4 * b + 2 * e + 1] * 2.0f * __builtin_bit_cast(float, rr & 0xFFFF0000u));
+              }
+              mine[b] = make_uint2(v[0], v[1]);
+            }
           } else {
             float x[4][4];   // the stored activation of features 8b + 4h + 0..3
             bool tiny = false;   // a subnormal stored s (the raw square root flushes it)
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
-              const int64_t f = f32 + 8 * b + 4 * lhalf;
+              const int64_t f = f32 + 8 * b + 4 * lh;
               uint2 a = make_uint2(0u, 0u);
               if (t < g.N && f < g.f_valid) a = *(const uint2*)(g.act + t * g.ld_act + f);
 #pragma unroll
@@ -930,7 +973,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             hi[e] = s1[0];
             hi[2 + e] = s1[1];
           }
-          const int64_t f = f32 + 16 * lhalf;
+          const int64_t f = f32 + 16 * lh;
           if (t < g.N) {
             uint16_t* dst = (Cfg::EPI == EPI_ACT_DENSE ? g.act : g.dact) + t * g.ld_act + f;
             if (f + 8 <= g.f_valid) *(uint4*)dst = make_uint4(lo[0], lo[1], lo[2], lo[3]);
@@ -1123,7 +1166,11 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     // The checked path (edge tiles, tail steps) passes k0 and the lane index
     // through an empty asm so that its addresses are formed afresh rather
     // than kept in loop-carried registers across the main loop.
+    // EPI_DH_STE: steps nsteps .. 2 nsteps - 1 are the K steps of (A2, B2).
     auto issue_a = [&](int64_t m0, int s_in, int step, uint32_t a_off) __attribute__((always_inline)) {
+      const bool second = TWO && step >= nsteps;
+      if (second) step -= nsteps;
+      const uint16_t* pa = second ? g.A2 : g.A;
       const int64_t k0 = kbeg + (int64_t)step * BK;
       const uint32_t base = smem_lds + a_off;
       if (step < s_in) {
@@ -1133,7 +1180,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           TMeta::template issue_fast<0, LM>((const char*)(g.Am + tiled_step<8>(m0, k0, g.tok, g.ldam)), offM,
                                             base + Cfg::A_BYTES, wave);
         } else {
-          TA::template issue_fast<0, LA>(TA::step_base(g.A, g.lda, m0, k0), offA, base, wave);
+          TA::template issue_fast<0, LA>(TA::step_base(pa, g.lda, m0, k0), offA, base, wave);
           if constexpr (SPARSE)
             TMeta::template issue_fast<0, LM>(TMeta::step_base(g.Am, g.ldam, m0, k0), offM, base + Cfg::A_BYTES, wave);
         }
@@ -1146,20 +1193,23 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           TA::template issue<0, LA>(g.A, g.lda, m0, g.m_valid, kc, g.ka_valid, base, wave, lc, tk);
           TMeta::template issue<0, LM>(g.Am, g.ldam, m0, g.m_valid, kc, g.ka_valid, base + Cfg::A_BYTES, wave, lc, tk);
         } else {
-          TA::template issue<0, LA>(g.A, g.lda, m0, g.m_valid, kc, g.ka_valid, base, wave, lc);
+          TA::template issue<0, LA>(pa, g.lda, m0, g.m_valid, kc, g.ka_valid, base, wave, lc);
         }
       }
     };
     auto issue_b = [&](int64_t n0, int s_in, int step, uint32_t b_off) __attribute__((always_inline)) {
+      const bool second = TWO && step >= nsteps;
+      if (second) step -= nsteps;
+      const uint16_t* pb = second ? g.B2 : g.B;
       const int64_t k0 = kbeg + (int64_t)step * BK;
       const uint32_t base = smem_lds + b_off;
       if (step < s_in) {
-        TB::template issue_fast<0, LB>(TB::step_base(g.B, g.ldb, n0, k0), offB, base, wave);
+        TB::template issue_fast<0, LB>(TB::step_base(pb, g.ldb, n0, k0), offB, base, wave);
       } else {
         int64_t kc = uniform_i64(k0);
         int lc = lane;
         asm volatile("" : "+s"(kc), "+v"(lc));
-        TB::template issue<0, LB>(g.B, g.ldb, n0, g.N, kc, g.kb_valid, base, wave, lc);
+        TB::template issue<0, LB>(pb, g.ldb, n0, g.N, kc, g.kb_valid, base, wave, lc);
       }
     };
 
@@ -1189,16 +1239,16 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     };
     load_next();
     // Lookahead step x (relative to the current tile's step 0) lies in this
-    // tile (x < nsteps) or in the next one; issue its A / B part if it exists.
+    // tile (x < tsteps) or in the next one; issue its A / B part if it exists.
     auto ahead_a = [&](int x, uint32_t a_off) __attribute__((always_inline)) {
-      const bool here = x < nsteps;
-      if (here || (has_next && x - nsteps < nsteps)) issue_a(here ? m0 : nm0, here ? s_in : ns_in, here ? x : x - nsteps, a_off);
+      const bool here = x < tsteps;
+      if (here || (has_next && x - tsteps < tsteps)) issue_a(here ? m0 : nm0, here ? s_in : ns_in, here ? x : x - tsteps, a_off);
     };
     auto ahead_b = [&](int x, uint32_t b_off) __attribute__((always_inline)) {
-      const bool here = x < nsteps;
-      if (here || (has_next && x - nsteps < nsteps)) issue_b(here ? n0 : nn0, here ? s_in : ns_in, here ? x : x - nsteps, b_off);
+      const bool here = x < tsteps;
+      if (here || (has_next && x - tsteps < tsteps)) issue_b(here ? n0 : nn0, here ? s_in : ns_in, here ? x : x - tsteps, b_off);
     };
-    auto exists = [&](int x) __attribute__((always_inline)) { return x < nsteps || (has_next && x - nsteps < nsteps); };
+    auto exists = [&](int x) __attribute__((always_inline)) { return x < tsteps || (has_next && x - tsteps < tsteps); };
 
     if constexpr (Cfg::DEEP != 0) {
       // The deep operand's stage of global step q is q % 3, the other's q % 2;
@@ -1221,7 +1271,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       ahead_deep(1, 1);
       for (;;) {
         zero_acc();
-        for (int s = 0; s < nsteps; ++s) {
+        for (int s = 0; s < tsteps; ++s) {
           // Step s needs both operands' step s; the loads issued after the
           // shallow operand's step s are the deep one's step s+1 (issued with
           // it at step s-1).  At a tile's first step the previous epilogue's
@@ -1234,10 +1284,11 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           ahead_shallow(s + 1, gs + s + 1);
           ahead_deep(s + 2, gs + s + 2);
           compute(smem + a_off(gs + s), smem + b_off(gs + s), [](int) {});
+          if (TWO && s == nsteps - 1) stash_h();
         }
         epilogue(m0, n0, smem, [] {});
         if (!has_next) break;
-        gs += nsteps;
+        gs += tsteps;
         tile = next;
         m0 = nm0;
         n0 = nn0;
@@ -1306,9 +1357,10 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         ahead_a(p, st_off(p));
         ahead_b(p, st_off(p) + Cfg::A_PART);
       }
+      static_assert(!TWO || !Cfg::PRE_S, "two operand pairs with a plain epilogue");
       for (;;) {
         zero_acc();
-        for (int s = 0; s < nsteps; ++s) {
+        for (int s = 0; s < tsteps; ++s) {
           // wait for this wave's loads of step s.  The loads of the up to
           // STAGES - 2 later steps already issued (after those of s: memory
           // operations complete in issue order) may stay in flight.  At a
@@ -1337,6 +1389,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           }
           const char* st = smem + st_off(gs + s);
           compute(st, st + Cfg::A_PART, [](int) {});
+          if (TWO && s == nsteps - 1) stash_h();
         }
         if constexpr (Cfg::PRE_S) {
           // the next tile's first step goes to the buffer the last step read
@@ -1352,11 +1405,11 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
               wait_vmcnt<0>();
           });
         } else {
-          const int last = nsteps > 0 ? (gs + nsteps - 1) % STAGES : 0;
+          const int last = tsteps > 0 ? (gs + tsteps - 1) % STAGES : 0;
           epilogue(m0, n0, smem + last * Cfg::STAGE, [] {});
         }
         if (!has_next) break;
-        gs += Cfg::PRE_S ? nsteps - 1 : nsteps;
+        gs += Cfg::PRE_S ? nsteps - 1 : tsteps;
         tile = next;
         m0 = nm0;
         n0 = nn0;

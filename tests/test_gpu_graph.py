@@ -61,3 +61,40 @@ def test_graph_replays_match_eager(name, T, mode):
         torch.cuda.synchronize()
         for k, v in outs.items():
             assert torch.equal(v, ref[k]), (rep, k)
+
+
+@pytest.mark.parametrize("name,T", [(None, 300), ("llama1b", 512), ("llama1b", 4096)])
+def test_graph_replays_noalloc_forward(name, T):
+    """The no-allocation forward (its workspace the library's static scratch)
+    captured in a graph with nothing but the caller's inputs and outputs:
+    every replay, with eager work between them, equals the eager result and
+    the workspace forward's, bit for bit."""
+    bits = config_inputs(name, T=T) if name else ffn_inputs(T, 128, 264, 32, seed_base=19)
+    t = {k: dev_bf16(v) for k, v in bits.items()}
+    ref = elas.elas_lowrank_ffn_fwd(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"])
+    out = {k: torch.empty_like(v) for k, v in ref.items()}
+
+    def fwd():
+        elas.elas_lowrank_ffn_fwd_noalloc(t["x"], t["U_up"], t["V_up"], t["U_down"], t["V_down"], out=out)
+
+    fwd()                                   # first call on the device: looks the scratch up, outside the capture
+    torch.cuda.synchronize()
+    for k in ref:
+        assert torch.equal(out[k], ref[k]), k
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fwd()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        fwd()
+    for rep in range(3):
+        for v in out.values():
+            v.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for k in ref:
+            assert torch.equal(out[k], ref[k]), (rep, k)
