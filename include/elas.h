@@ -238,7 +238,8 @@ int elas_lowrank_ffn_fwd_noalloc(const uint16_t* x, const uint16_t* U_up, const 
  *     from the stored bf16 s.  The full-width activation is never read:
  *     dU_down = S^T dZ and dV_up = P^T dH use the compressed form.
  *   ELAS_BWD_STE (after a sparse forward): Eq. 4, dH = dS * 2 relu(h) at every
- *     position; relu(h) is recomputed from P and V_up.
+ *     position; relu(h) = relu(bf16(P V_up)) is recomputed tile by tile inside
+ *     the dH kernel (no d_ff-wide activation is stored).
  *   ELAS_MODE_DENSE (after a dense forward): dH = dS * 2 relu(h), dense.
  * Rounding points: dZ, dH, dP and dx are rounded to bf16.
  * flags: 0, ELAS_BWD_STE or ELAS_MODE_DENSE (the forward's mode).
