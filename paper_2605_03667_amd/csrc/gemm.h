@@ -69,6 +69,9 @@ struct GemmArgs {
   int64_t ldam;        // byte pitch of the metadata
   const uint16_t* B;   // OP_K [N x K], OP_T [K x N]
   int64_t ldb;
+  // b_nsk > 0: B (OP_K) is blocked (blocked_index below) with b_nsk K blocks
+  // per row panel, zero-padded, and ldb is 64; every B load is unchecked.
+  int64_t b_nsk;
   // EPI_DH_STE: the second operand pair (same shapes and pitches as A, B).
   // The tile's contraction runs over (A, B) first, whose product is H^T, then
   // over (A2, B2), whose product is dS^T.
@@ -118,6 +121,15 @@ struct GemmArgs {
 // values or 8 metadata bytes: 64 features); block (row block, entry block)
 // holds its R rows x BW entries row-major and contiguously, blocks ordered by
 // row block, then entry block.  Index of entry j of row t:
+// Blocked layout of a K-contiguous [N x K] operand: 256-row panels, each cut
+// into 64-wide K blocks stored contiguously ([256 x 64] row-major, 32 KB),
+// blocks ordered by panel, then K block; nsk = K blocks per panel (K padded
+// to 64, N to 256, with zeros).  One K step of a 256-row (or 128-row) tile is
+// then one contiguous piece of memory.
+__host__ __device__ inline int64_t blocked_index(int64_t n, int64_t k, int64_t nsk) {
+  return (((n >> 8) * nsk + (k >> 6)) << 14) + ((n & 255) << 6) + (k & 63);
+}
+
 template <int BW>
 __device__ __forceinline__ int64_t tiled_index(int64_t t, int64_t j, int64_t tok, int64_t ld) {
   const int64_t tb = t >> 8;
@@ -201,6 +213,10 @@ struct GemmCfg {
   static_assert(!STAGED_EPI || (BM_ == 256 && BN_ * BM_ <= STAGE && DIRECT), "staged epilogue layout");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
   static_assert(EPI_ != EPI_DH_STE || AMODE_ != OP_TSP, "two operand pairs: direct staging");
+  // a blocked B (GemmArgs::b_nsk) needs 128-byte LDS rows of B (64 K per
+  // step); only the plain-output products take one, and the other kernels are
+  // compiled without the branch
+  static constexpr bool B_BLOCKABLE = !B_KM && B_ROWB == 128 && (EPI_ == EPI_BF16 || EPI_ == EPI_F32);
 };
 
 // LDS chunk swizzle.  Fragment reads touch 8 consecutive rows at one chunk;
@@ -1203,8 +1219,10 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       const uint16_t* pb = second ? g.B2 : g.B;
       const int64_t k0 = kbeg + (int64_t)step * BK;
       const uint32_t base = smem_lds + b_off;
-      if (step < s_in) {
-        TB::template issue_fast<0, LB>(TB::step_base(pb, g.ldb, n0, k0), offB, base, wave);
+      const bool bblk = Cfg::B_BLOCKABLE && g.b_nsk > 0;
+      if (step < s_in || bblk) {
+        const char* sb = bblk ? (const char*)(pb + blocked_index(n0, k0, g.b_nsk)) : TB::step_base(pb, g.ldb, n0, k0);
+        TB::template issue_fast<0, LB>(sb, offB, base, wave);
       } else {
         int64_t kc = uniform_i64(k0);
         int lc = lane;

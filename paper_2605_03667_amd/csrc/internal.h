@@ -12,6 +12,7 @@ namespace elas {
 inline int64_t vals_ld(int64_t n) { return 32 * ((n + 63) / 64); }
 inline int64_t meta_ld(int64_t n) { return 8 * ((n + 63) / 64); }
 inline int64_t pad64(int64_t n) { return 64 * ((n + 63) / 64); }
+inline int64_t pad256(int64_t n) { return 256 * ((n + 255) / 256); }
 
 // timing.hip: brackets one launch with events when timing is enabled, and
 // synchronises after it in the ELAS_DEBUG_SYNC mode (the first failure of
