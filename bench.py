@@ -60,6 +60,8 @@ def algorithmic_flops(tag: str, T: int, d: int, F: int, r: int) -> float | None:
         "k4_down_gemm": 2 * T * r * d, "b1_dZ": 2 * T * d * r, "b2_dV_down": 2 * T * d * r,
         "b3_dH_masked": T * r * F, "b4_dU_down": T * r * F, "b5_spmm_dP": T * r * F, "b6_dV_up": T * r * F,
         "b7_dU_up": 2 * T * d * r, "b8_dx": 2 * T * d * r,
+        # straight-through backward (Eq. 4): dH, dP and dV_up at every position
+        "b3_dH_ste": 2 * T * r * F, "b5_dP_dense": 2 * T * r * F, "b6_dV_up_dense": 2 * T * r * F,
     }
     v = table.get(tag)
     return None if v is None else float(v)
@@ -75,6 +77,8 @@ def executed_flops(tag: str, T: int, d: int, F: int, r: int) -> float | None:
         return 2.0 * T * r * Fp
     if tag in ("k3_spmm_down", "b3_dH_masked", "b4_dU_down", "b5_spmm_dP", "b6_dV_up"):
         return 2.0 * T * r * Fp
+    if tag == "b3_dH_ste":   # relu(h) recomputed in the same tile: h and dS, both dense
+        return 4.0 * T * r * Fp
     return a
 
 
@@ -94,6 +98,8 @@ def algorithmic_bytes(tag: str, T: int, d: int, F: int, r: int) -> float | None:
         "b3_dH_masked": 2 * (T * r + F * r) + S + dH, "b4_dU_down": S + 2 * T * r + 4 * F * r,
         "b5_spmm_dP": dH + meta + 2 * (r * F + T * r), "b6_dV_up": dH + meta + 2 * T * r + 4 * r * F,
         "b7_dU_up": 2 * (T * d + T * r) + 4 * d * r, "b8_dx": 2 * (T * r + d * r + T * d),
+        "b3_dH_ste": 2 * (2 * T * r + 2 * F * r) + 2 * T * F, "b5_dP_dense": 2 * (T * F + r * F + T * r),
+        "b6_dV_up_dense": 2 * (T * F + T * r) + 4 * r * F,
     }
     v = table.get(tag)
     return None if v is None else float(v)
@@ -464,6 +470,26 @@ def config_steps(name: str, steps: int, warmup: int, bwd_flags: int = 0) -> dict
     ms = a.elapsed_time(b) / steps
     out = {"tokens_per_s": round(T / (ms / 1e3), 1), "ms_per_step": round(ms, 4), "steps": steps,
            "T": T, "d": d, "d_ff": F, "r": r}
+    if bwd_flags:
+        # per-kernel table of this line: a separate pass with events around every launch
+        elas.elas_timing_only(None)
+        elas.elas_timing_enable(True)
+        torch.cuda.synchronize()
+        for _ in range(steps):
+            step()
+        torch.cuda.synchronize()
+        elas.elas_timing_enable(False)
+        ks = {}
+        for tag, (n, kms) in sorted(elas.elas_timing_collect().items(), key=lambda kv: -kv[1][1]):
+            us = kms / n * 1e3
+            row = {"launches": n, "avg_us": round(us, 2)}
+            fl = algorithmic_flops(tag, T, d, F, r)
+            if fl is not None:
+                row["alg_tflops"] = round(fl / (us * 1e-6) / 1e12, 1)
+                ex = executed_flops(tag, T, d, F, r)
+                row["exec_tflops"] = round(ex / (us * 1e-6) / 1e12, 1)
+            ks[tag] = row
+        out["kernels"] = ks
     del t, ws_f, ws_b, saved, grads
     torch.cuda.empty_cache()
     return out
