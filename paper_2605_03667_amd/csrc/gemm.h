@@ -1256,17 +1256,108 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       }
     };
     load_next();
+    // Issue cursors.  Every operand's source address is linear in the step
+    // over a tile's unchecked steps (a prefix of its steps), so each operand
+    // keeps the address of the next step it issues, the per-step stride and
+    // the number of unchecked steps left.  At a tile's step 0 the general
+    // address code sets the cursor up; an unchecked step is then the DMAs plus
+    // a pointer add.  Eight waves run their scalar code on the CU's one
+    // scalar unit, so the per-step scalar instruction count is what bounds
+    // the copy issue.  (The two-pair kernel and the dense-activation
+    // epilogues keep the general path: with the cursors the compiler
+    // duplicates their main loop and spills.)
+    constexpr bool LEAN = !TWO && Cfg::EPI != EPI_ACT_DENSE && Cfg::EPI != EPI_DH_DENSE;
+    // A 2:4 operand's metadata advances by 1/8 of its kept values' stride
+    // (tiled: 8 R against 64 R bytes; rows: BK/8 against BK bytes).
+    const char* ca_p = nullptr;   // A (kept values for a 2:4 operand)
+    const char* ca_m = nullptr;   // its metadata
+    uint32_t ca_st = 0;
+    int ca_n = 0;
+    const char* cb_p = nullptr;
+    uint32_t cb_st = 0;
+    int cb_n = 0;
+    auto a_src = [&](int64_t tm0, int64_t k0, const char*& pv, const char*& pm) __attribute__((always_inline)) {
+      if (SPARSE && g.a_tiled) {
+        pv = (const char*)(g.A + tiled_step<32>(tm0, k0, g.tok, g.lda));
+        pm = (const char*)(g.Am + tiled_step<8>(tm0, k0, g.tok, g.ldam));
+      } else {
+        pv = TA::step_base(g.A, g.lda, tm0, k0);
+        if constexpr (SPARSE) pm = TMeta::step_base(g.Am, g.ldam, tm0, k0);
+      }
+    };
+    auto b_src = [&](int64_t tn0, int64_t k0) __attribute__((always_inline)) {
+      const bool bblk = Cfg::B_BLOCKABLE && g.b_nsk > 0;
+      return bblk ? (const char*)(g.B + blocked_index(tn0, k0, g.b_nsk)) : TB::step_base(g.B, g.ldb, tn0, k0);
+    };
+    auto setup_a = [&](int64_t tm0, int tin) __attribute__((always_inline)) {
+      const char *v0 = nullptr, *m0p = nullptr, *v1 = nullptr, *m1p = nullptr;
+      a_src(tm0, kbeg, v0, m0p);
+      a_src(tm0, kbeg + BK, v1, m1p);
+      (void)m1p;
+      ca_p = (const char*)uniform_ptr(v0);
+      ca_st = __builtin_amdgcn_readfirstlane((uint32_t)(v1 - v0));
+      if constexpr (SPARSE) ca_m = (const char*)uniform_ptr(m0p);
+      ca_n = tin;
+    };
+    auto setup_b = [&](int64_t tn0, int tin) __attribute__((always_inline)) {
+      const char* p0 = b_src(tn0, kbeg);
+      cb_p = (const char*)uniform_ptr(p0);
+      cb_st = __builtin_amdgcn_readfirstlane((uint32_t)(b_src(tn0, kbeg + BK) - p0));
+      cb_n = (Cfg::B_BLOCKABLE && g.b_nsk > 0) ? nsteps : tin;
+    };
     // Lookahead step x (relative to the current tile's step 0) lies in this
     // tile (x < tsteps) or in the next one; issue its A / B part if it exists.
     auto ahead_a = [&](int x, uint32_t a_off) __attribute__((always_inline)) {
       const bool here = x < tsteps;
-      if (here || (has_next && x - tsteps < tsteps)) issue_a(here ? m0 : nm0, here ? s_in : ns_in, here ? x : x - tsteps, a_off);
+      if (!(here || (has_next && x - tsteps < tsteps))) return;
+      if constexpr (LEAN) {
+        if (x == 0 || x == tsteps) setup_a(here ? m0 : nm0, here ? s_in : ns_in);
+        if (ca_n > 0) {
+          const uint32_t base = smem_lds + a_off;
+          TA::template issue_fast<0, LA>(ca_p, offA, base, wave);
+          if constexpr (SPARSE) {
+            TMeta::template issue_fast<0, LM>(ca_m, offM, base + Cfg::A_BYTES, wave);
+            ca_m += ca_st >> 3;
+          }
+          ca_p += ca_st;
+          --ca_n;
+          return;
+        }
+      }
+      issue_a(here ? m0 : nm0, here ? s_in : ns_in, here ? x : x - tsteps, a_off);
     };
     auto ahead_b = [&](int x, uint32_t b_off) __attribute__((always_inline)) {
       const bool here = x < tsteps;
-      if (here || (has_next && x - tsteps < tsteps)) issue_b(here ? n0 : nn0, here ? s_in : ns_in, here ? x : x - tsteps, b_off);
+      if (!(here || (has_next && x - tsteps < tsteps))) return;
+      if constexpr (LEAN) {
+        if (x == 0 || x == tsteps) setup_b(here ? n0 : nn0, here ? s_in : ns_in);
+        if (cb_n > 0) {
+          TB::template issue_fast<0, LB>(cb_p, offB, smem_lds + b_off, wave);
+          cb_p += cb_st;
+          --cb_n;
+          return;
+        }
+      }
+      issue_b(here ? n0 : nn0, here ? s_in : ns_in, here ? x : x - tsteps, b_off);
     };
     auto exists = [&](int x) __attribute__((always_inline)) { return x < tsteps || (has_next && x - tsteps < tsteps); };
+    // Steady-state issue from the cursors: the caller guarantees an unchecked
+    // step of the current tile (so the counts are positive).
+    auto fast_a = [&](uint32_t a_off) __attribute__((always_inline)) {
+      const uint32_t base = smem_lds + a_off;
+      TA::template issue_fast<0, LA>(ca_p, offA, base, wave);
+      if constexpr (SPARSE) {
+        TMeta::template issue_fast<0, LM>(ca_m, offM, base + Cfg::A_BYTES, wave);
+        ca_m += ca_st >> 3;
+      }
+      ca_p += ca_st;
+      --ca_n;
+    };
+    auto fast_b = [&](uint32_t b_off) __attribute__((always_inline)) {
+      TB::template issue_fast<0, LB>(cb_p, offB, smem_lds + b_off, wave);
+      cb_p += cb_st;
+      --cb_n;
+    };
 
     if constexpr (Cfg::DEEP != 0) {
       // The deep operand's stage of global step q is q % 3, the other's q % 2;
@@ -1290,6 +1381,32 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       for (;;) {
         zero_acc();
         for (int s = 0; s < tsteps; ++s) {
+          if constexpr (LEAN) {
+            // Steady state: steps 1 .. s_in - 3 issue unchecked steps s+1 and
+            // s+2 of this tile from the cursors; ring positions advance
+            // without a modulo.
+            if (s == 1) {
+              int r3 = (gs + 1) % 3, r2 = (gs + 1) & 1;   // (gs + s) mod 3, mod 2
+              for (; s < s_in - 2; ++s) {
+                wait_vmcnt<LOADS_DEEP>();
+                lds_barrier();
+                const int r3n2 = r3 == 0 ? 2 : r3 - 1;   // (gs + s + 2) mod 3
+                const int d_cur = DA ? r3 : r2, a_r = DA ? r3 : r2, b_r = DA ? r2 : r3;
+                (void)d_cur;
+                if constexpr (DA) {
+                  fast_b(NA * Cfg::A_PART + (r2 ^ 1) * Cfg::B_BYTES);
+                  fast_a(r3n2 * Cfg::A_PART);
+                } else {
+                  fast_a((r2 ^ 1) * Cfg::A_PART);
+                  fast_b(NA * Cfg::A_PART + r3n2 * Cfg::B_BYTES);
+                }
+                compute(smem + a_r * Cfg::A_PART, smem + NA * Cfg::A_PART + b_r * Cfg::B_BYTES, [](int) {});
+                r3 = r3 == 2 ? 0 : r3 + 1;
+                r2 ^= 1;
+              }
+              if (s >= tsteps) break;
+            }
+          }
           // Step s needs both operands' step s; the loads issued after the
           // shallow operand's step s are the deep one's step s+1 (issued with
           // it at step s-1).  At a tile's first step the previous epilogue's
@@ -1379,6 +1496,27 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       for (;;) {
         zero_acc();
         for (int s = 0; s < tsteps; ++s) {
+          if constexpr (LEAN) {
+            // Steady state: steps 1 .. s_in - STAGES + 1 issue unchecked
+            // steps of this tile from the cursors (the later steps already
+            // issued all exist, so the wait count is fixed); ring positions
+            // advance without a modulo.
+            if (s == 1) {
+              constexpr int W = STAGES >= 4 ? 2 * LOADS : STAGES == 3 ? LOADS : 0;
+              int rc = (gs + 1) % STAGES;   // stage of step s
+              for (; s < s_in - (STAGES - 1); ++s) {
+                wait_vmcnt<W>();
+                lds_barrier();
+                const int ri = rc == 0 ? STAGES - 1 : rc - 1;   // stage of step s + STAGES - 1
+                fast_a(ri * Cfg::STAGE);
+                fast_b(ri * Cfg::STAGE + Cfg::A_PART);
+                const char* st = smem + rc * Cfg::STAGE;
+                compute(st, st + Cfg::A_PART, [](int) {});
+                rc = rc == STAGES - 1 ? 0 : rc + 1;
+              }
+              if (s >= tsteps) break;
+            }
+          }
           // wait for this wave's loads of step s.  The loads of the up to
           // STAGES - 2 later steps already issued (after those of s: memory
           // operations complete in issue order) may stay in flight.  At a
