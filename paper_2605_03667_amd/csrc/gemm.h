@@ -1393,14 +1393,13 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
                 const int r3n2 = r3 == 0 ? 2 : r3 - 1;   // (gs + s + 2) mod 3
                 const int d_cur = DA ? r3 : r2, a_r = DA ? r3 : r2, b_r = DA ? r2 : r3;
                 (void)d_cur;
-                if constexpr (DA) {
-                  fast_b(NA * Cfg::A_PART + (r2 ^ 1) * Cfg::B_BYTES);
-                  fast_a(r3n2 * Cfg::A_PART);
-                } else {
-                  fast_a((r2 ^ 1) * Cfg::A_PART);
-                  fast_b(NA * Cfg::A_PART + r3n2 * Cfg::B_BYTES);
-                }
+                // the shallow operand's step s+1 before this step's MFMAs (it
+                // is needed next step), the deep one's step s+2 after them
+                if constexpr (DA) fast_b(NA * Cfg::A_PART + (r2 ^ 1) * Cfg::B_BYTES);
+                else fast_a((r2 ^ 1) * Cfg::A_PART);
                 compute(smem + a_r * Cfg::A_PART, smem + NA * Cfg::A_PART + b_r * Cfg::B_BYTES, [](int) {});
+                if constexpr (DA) fast_a(r3n2 * Cfg::A_PART);
+                else fast_b(NA * Cfg::A_PART + r3n2 * Cfg::B_BYTES);
                 r3 = r3 == 2 ? 0 : r3 + 1;
                 r2 ^= 1;
               }
@@ -1508,10 +1507,19 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
                 wait_vmcnt<W>();
                 lds_barrier();
                 const int ri = rc == 0 ? STAGES - 1 : rc - 1;   // stage of step s + STAGES - 1
-                fast_a(ri * Cfg::STAGE);
-                fast_b(ri * Cfg::STAGE + Cfg::A_PART);
                 const char* st = smem + rc * Cfg::STAGE;
+                if constexpr (STAGES == 2) {
+                  fast_a(ri * Cfg::STAGE);
+                  fast_b(ri * Cfg::STAGE + Cfg::A_PART);
+                }
                 compute(st, st + Cfg::A_PART, [](int) {});
+                if constexpr (STAGES > 2) {
+                  // copies of step s + STAGES - 1 after this step's MFMAs: its
+                  // stage was last read in step s - 1 (before the barrier), and
+                  // it has a whole step to land
+                  fast_a(ri * Cfg::STAGE);
+                  fast_b(ri * Cfg::STAGE + Cfg::A_PART);
+                }
                 rc = rc == STAGES - 1 ? 0 : rc + 1;
               }
               if (s >= tsteps) break;
@@ -1602,6 +1610,20 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
         a_steps_in = k_in <= 0 ? 0 : (int)(k_in / BK < ns ? k_in / BK : ns);
       }
       a_steps_in = __builtin_amdgcn_readfirstlane(a_steps_in);
+      // Copy cursors (the scalar code of eight waves shares one scalar unit,
+      // so the unchecked steps avoid the general address arithmetic).  In
+      // the tiled layout a step's 64 token rows of kept values (metadata) lie
+      // 4096 (512) bytes after the previous step's inside a 256-row block; at
+      // a block boundary the next block's rows follow 512 lda - 3 * 4096
+      // (256 ldam - 3 * 512) bytes on (full blocks: R = 256).  B advances BK
+      // rows (K-major) or BK elements.
+      static_assert(BK == 64, "64 token rows per step");
+      const char* cv = (const char*)uniform_ptr(g.A + tiled_step<32>(kb, m0, g.tok, g.lda));
+      const char* cm = (const char*)uniform_ptr(g.Am + tiled_step<8>(kb, m0, g.tok, g.ldam));
+      const int64_t jv = uniform_i64(512 * g.lda - 3 * 4096), jm = uniform_i64(256 * g.ldam - 3 * 512);
+      uint32_t tpos = __builtin_amdgcn_readfirstlane((uint32_t)(kb & 255));   // token row in its block of the next load
+      const char* cb = (const char*)uniform_ptr(TB::step_base(g.B, g.ldb, n0, kb));
+      const uint32_t sb = __builtin_amdgcn_readfirstlane((uint32_t)(TB::step_base(g.B, g.ldb, n0, kb + BK) - TB::step_base(g.B, g.ldb, n0, kb)));
       auto load_a = [&](int step) __attribute__((always_inline)) {
         const int64_t k0 = kb + (int64_t)step * BK;
         if (step < a_steps_in) {
@@ -1611,8 +1633,11 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
           int tc = tid;
           asm volatile("" : "+v"(tc));
           StagerKMSP<BM, NT>::lane_offs(tc, aov, aom);
-          sa.load_fast((const char*)(g.A + tiled_step<32>(k0, m0, g.tok, g.lda)),
-                       (const char*)(g.Am + tiled_step<8>(k0, m0, g.tok, g.ldam)), aov, aom);
+          sa.load_fast(cv, cm, aov, aom);
+          tpos = (tpos + 64) & 255;
+          const bool cross = tpos == 0;
+          cv += cross ? jv : 4096;
+          cm += cross ? jm : 512;
         } else {
           int64_t kc = uniform_i64(k0);   // addresses formed afresh (see the direct path)
           int tc = tid;
@@ -1623,9 +1648,10 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       auto issue_b = [&](int step) __attribute__((always_inline)) {
         const int64_t k0 = kb + (int64_t)step * BK;
         const uint32_t base = smem_lds + (uint32_t)((step & 1) * Cfg::STAGE) + Cfg::A_BYTES;
-        if (step < b_steps_in)
-          TB::template issue_fast<0, TB::PER_WAVE>(TB::step_base(g.B, g.ldb, n0, k0), offB, base, wave);
-        else
+        if (step < b_steps_in) {
+          TB::template issue_fast<0, TB::PER_WAVE>(cb, offB, base, wave);
+          cb += sb;
+        } else
           TB::template issue<0, TB::PER_WAVE>(g.B, g.ldb, n0, g.N, k0, g.kb_valid, base, wave, lane);
       };
       if (ns > 0) {
