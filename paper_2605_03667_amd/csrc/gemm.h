@@ -1391,8 +1391,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
                 wait_vmcnt<LOADS_DEEP>();
                 lds_barrier();
                 const int r3n2 = r3 == 0 ? 2 : r3 - 1;   // (gs + s + 2) mod 3
-                const int d_cur = DA ? r3 : r2, a_r = DA ? r3 : r2, b_r = DA ? r2 : r3;
-                (void)d_cur;
+                const int a_r = DA ? r3 : r2, b_r = DA ? r2 : r3;   // stages of step s
                 // the shallow operand's step s+1 before this step's MFMAs (it
                 // is needed next step), the deep one's step s+2 after them
                 if constexpr (DA) fast_b(NA * Cfg::A_PART + (r2 ^ 1) * Cfg::B_BYTES);
