@@ -3,7 +3,7 @@
 bf16 is the upper half of an IEEE binary32: 1 sign bit, 8 exponent bits and 7
 fraction bits, so it has binary32's exponent range (normal numbers from 2^-126,
 subnormal spacing 2^-133) with 8 significant bits.  The paper trains in BF16
-(Sec. 4.1); every stored bf16 value in this build is produced by rounding to
+(Sec. 4.1); every bf16 value the library stores is produced by rounding to
 nearest, ties to even.
 """
 from __future__ import annotations
