@@ -27,7 +27,7 @@ def _shapes(n, seed):
 
 
 @pytest.mark.parametrize("mode", ["sparse", "dense", "ste"])
-@pytest.mark.parametrize("T,d,F,r", _shapes(8, 2026))
+@pytest.mark.parametrize("T,d,F,r", _shapes(24, 2026))
 def test_random_shapes(T, d, F, r, mode):
     bits = ffn_inputs(T, d, F, r, seed_base=T + d + F + r)
     f, b = offn.run(bits, sparse=(mode != "dense"), ste=(mode == "ste"))
