@@ -1268,7 +1268,9 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     // duplicates their main loop and spills.)
     constexpr bool LEAN = !TWO && Cfg::EPI != EPI_ACT_DENSE && Cfg::EPI != EPI_DH_DENSE;
     // A 2:4 operand's metadata advances by 1/8 of its kept values' stride
-    // (tiled: 8 R against 64 R bytes; rows: BK/8 against BK bytes).
+    // (tiled: 8 R against 64 R bytes; rows: BK/8 against BK bytes).  A stride
+    // is at most BK rows of a pitch the entry points bound by 65536 elements
+    // (about 8 MB), so 32 bits hold it.
     const char* ca_p = nullptr;   // A (kept values for a 2:4 operand)
     const char* ca_m = nullptr;   // its metadata
     uint32_t ca_st = 0;
