@@ -1263,10 +1263,11 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     // address code sets the cursor up; an unchecked step is then the DMAs plus
     // a pointer add.  Eight waves run their scalar code on the CU's one
     // scalar unit, so the per-step scalar instruction count is what bounds
-    // the copy issue.  (The two-pair kernel and the dense-activation
-    // epilogues keep the general path: with the cursors the compiler
-    // duplicates their main loop and spills.)
-    constexpr bool LEAN = !TWO && Cfg::EPI != EPI_ACT_DENSE && Cfg::EPI != EPI_DH_DENSE;
+    // the copy issue.  The two-pair kernel sets its cursors up again at the
+    // second pair's step 0.  (The dense-activation epilogues keep the general
+    // path: with the cursors the compiler duplicates their main loop and
+    // spills.)
+    constexpr bool LEAN = Cfg::EPI != EPI_ACT_DENSE && Cfg::EPI != EPI_DH_DENSE;
     // A 2:4 operand's metadata advances by 1/8 of its kept values' stride
     // (tiled: 8 R against 64 R bytes; rows: BK/8 against BK bytes).  A stride
     // is at most BK rows of a pitch the entry points bound by 65536 elements
@@ -1278,42 +1279,48 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     const char* cb_p = nullptr;
     uint32_t cb_st = 0;
     int cb_n = 0;
-    auto a_src = [&](int64_t tm0, int64_t k0, const char*& pv, const char*& pm) __attribute__((always_inline)) {
+    auto a_src = [&](int64_t tm0, int64_t k0, bool second, const char*& pv, const char*& pm) __attribute__((always_inline)) {
       if (SPARSE && g.a_tiled) {
         pv = (const char*)(g.A + tiled_step<32>(tm0, k0, g.tok, g.lda));
         pm = (const char*)(g.Am + tiled_step<8>(tm0, k0, g.tok, g.ldam));
       } else {
-        pv = TA::step_base(g.A, g.lda, tm0, k0);
+        pv = TA::step_base(TWO && second ? g.A2 : g.A, g.lda, tm0, k0);
         if constexpr (SPARSE) pm = TMeta::step_base(g.Am, g.ldam, tm0, k0);
       }
     };
-    auto b_src = [&](int64_t tn0, int64_t k0) __attribute__((always_inline)) {
+    auto b_src = [&](int64_t tn0, int64_t k0, bool second) __attribute__((always_inline)) {
       const bool bblk = Cfg::B_BLOCKABLE && g.b_nsk > 0;
-      return bblk ? (const char*)(g.B + blocked_index(tn0, k0, g.b_nsk)) : TB::step_base(g.B, g.ldb, tn0, k0);
+      return bblk ? (const char*)(g.B + blocked_index(tn0, k0, g.b_nsk))
+                  : TB::step_base(TWO && second ? g.B2 : g.B, g.ldb, tn0, k0);
     };
-    auto setup_a = [&](int64_t tm0, int tin) __attribute__((always_inline)) {
+    auto setup_a = [&](int64_t tm0, int tin, bool second) __attribute__((always_inline)) {
       const char *v0 = nullptr, *m0p = nullptr, *v1 = nullptr, *m1p = nullptr;
-      a_src(tm0, kbeg, v0, m0p);
-      a_src(tm0, kbeg + BK, v1, m1p);
+      a_src(tm0, kbeg, second, v0, m0p);
+      a_src(tm0, kbeg + BK, second, v1, m1p);
       (void)m1p;
       ca_p = (const char*)uniform_ptr(v0);
       ca_st = __builtin_amdgcn_readfirstlane((uint32_t)(v1 - v0));
       if constexpr (SPARSE) ca_m = (const char*)uniform_ptr(m0p);
       ca_n = tin;
     };
-    auto setup_b = [&](int64_t tn0, int tin) __attribute__((always_inline)) {
-      const char* p0 = b_src(tn0, kbeg);
+    auto setup_b = [&](int64_t tn0, int tin, bool second) __attribute__((always_inline)) {
+      const char* p0 = b_src(tn0, kbeg, second);
       cb_p = (const char*)uniform_ptr(p0);
-      cb_st = __builtin_amdgcn_readfirstlane((uint32_t)(b_src(tn0, kbeg + BK) - p0));
+      cb_st = __builtin_amdgcn_readfirstlane((uint32_t)(b_src(tn0, kbeg + BK, second) - p0));
       cb_n = (Cfg::B_BLOCKABLE && g.b_nsk > 0) ? nsteps : tin;
     };
     // Lookahead step x (relative to the current tile's step 0) lies in this
     // tile (x < tsteps) or in the next one; issue its A / B part if it exists.
+    // A cursor is set up at step 0 of each operand pair of a tile.
+    auto pair_start = [&](int x) __attribute__((always_inline)) {
+      const int xs = x < tsteps ? x : x - tsteps;
+      return xs == 0 || (TWO && xs == nsteps);
+    };
     auto ahead_a = [&](int x, uint32_t a_off) __attribute__((always_inline)) {
       const bool here = x < tsteps;
       if (!(here || (has_next && x - tsteps < tsteps))) return;
       if constexpr (LEAN) {
-        if (x == 0 || x == tsteps) setup_a(here ? m0 : nm0, here ? s_in : ns_in);
+        if (pair_start(x)) setup_a(here ? m0 : nm0, here ? s_in : ns_in, (here ? x : x - tsteps) >= nsteps);
         if (ca_n > 0) {
           const uint32_t base = smem_lds + a_off;
           TA::template issue_fast<0, LA>(ca_p, offA, base, wave);
@@ -1332,7 +1339,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
       const bool here = x < tsteps;
       if (!(here || (has_next && x - tsteps < tsteps))) return;
       if constexpr (LEAN) {
-        if (x == 0 || x == tsteps) setup_b(here ? n0 : nn0, here ? s_in : ns_in);
+        if (pair_start(x)) setup_b(here ? n0 : nn0, here ? s_in : ns_in, (here ? x : x - tsteps) >= nsteps);
         if (cb_n > 0) {
           TB::template issue_fast<0, LB>(cb_p, offB, smem_lds + b_off, wave);
           cb_p += cb_st;
@@ -1387,9 +1394,13 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             // Steady state: steps 1 .. s_in - 3 issue unchecked steps s+1 and
             // s+2 of this tile from the cursors; ring positions advance
             // without a modulo.
-            if (s == 1) {
-              int r3 = (gs + 1) % 3, r2 = (gs + 1) & 1;   // (gs + s) mod 3, mod 2
-              for (; s < s_in - 2; ++s) {
+            if (s == 1 || (TWO && s == nsteps + 1)) {
+              // (two-pair kernel: each pair's run separately, so that the
+              // cursor set-up at the second pair's step 0 and stash_h at the
+              // first pair's last step stay in the general body)
+              const int s_end = (TWO && s > nsteps ? nsteps : 0) + s_in - 2;
+              int r3 = (gs + s) % 3, r2 = (gs + s) & 1;   // (gs + s) mod 3, mod 2
+              for (; s < s_end; ++s) {
                 wait_vmcnt<LOADS_DEEP>();
                 lds_barrier();
                 const int r3n2 = r3 == 0 ? 2 : r3 - 1;   // (gs + s + 2) mod 3
@@ -1501,10 +1512,11 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             // steps of this tile from the cursors (the later steps already
             // issued all exist, so the wait count is fixed); ring positions
             // advance without a modulo.
-            if (s == 1) {
+            if (s == 1 || (TWO && s == nsteps + 1)) {
               constexpr int W = STAGES >= 4 ? 2 * LOADS : STAGES == 3 ? LOADS : 0;
-              int rc = (gs + 1) % STAGES;   // stage of step s
-              for (; s < s_in - (STAGES - 1); ++s) {
+              const int s_end = (TWO && s > nsteps ? nsteps : 0) + s_in - (STAGES - 1);   // per operand pair
+              int rc = (gs + s) % STAGES;   // stage of step s
+              for (; s < s_end; ++s) {
                 wait_vmcnt<W>();
                 lds_barrier();
                 const int ri = rc == 0 ? STAGES - 1 : rc - 1;   // stage of step s + STAGES - 1
