@@ -1265,8 +1265,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
     // scalar unit, so the per-step scalar instruction count is what bounds
     // the copy issue.  The two-pair kernel sets its cursors up again at the
     // second pair's step 0.  (The dense-activation epilogues keep the general
-    // path: with the cursors the compiler duplicates their main loop and
-    // spills.)
+    // path: with the cursors they measured no faster.)
     constexpr bool LEAN = Cfg::EPI != EPI_ACT_DENSE && Cfg::EPI != EPI_DH_DENSE;
     // A 2:4 operand's metadata advances by 1/8 of its kept values' stride
     // (tiled: 8 R against 64 R bytes; rows: BK/8 against BK bytes).  A stride
