@@ -50,6 +50,7 @@
 #include "device.h"
 
 namespace elas {
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 
 enum OpMode { OP_K = 0, OP_T = 1, OP_SP = 2, OP_TSP = 3 };
 enum EpiMode {
@@ -928,7 +929,10 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
             }
           } else {
             float x[4][4];   // the stored activation of features 8b + 4h + 0..3
-            bool tiny = false;   // a subnormal stored s (the raw square root flushes it)
+            // a subnormal stored s (the raw square root flushes it): bit
+            // pattern v in [1, 0x7F], tested as (v - 1) mod 2^16 < 0x7F on the
+            // smallest of the lane's values (packed 16-bit integer arithmetic)
+            u16x2 vmin = {0xFFFFu, 0xFFFFu};
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
               const int64_t f = f32 + 8 * b + 4 * lh;
@@ -939,9 +943,10 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
                 const uint32_t w = e ? a.y : a.x;
                 x[b][2 * e] = __builtin_bit_cast(float, w << 16);
                 x[b][2 * e + 1] = __builtin_bit_cast(float, w & 0xFFFF0000u);
-                tiny |= __builtin_amdgcn_classf(x[b][2 * e], 0x80) | __builtin_amdgcn_classf(x[b][2 * e + 1], 0x80);
+                vmin = __builtin_elementwise_min(vmin, __builtin_bit_cast(u16x2, w) - (u16x2){1u, 1u});
               }
             }
+            const bool tiny = (vmin[0] < vmin[1] ? vmin[0] : vmin[1]) < 0x7Fu;
             if (g.act_square) {   // r = bf16(sqrt(s)) recovers relu(h) exactly
               float rt[4][4];
               if (__builtin_amdgcn_ballot_w64(tiny) == 0) {
@@ -1065,15 +1070,20 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const GemmArgs g) {
               const uint32_t w = *(const uint32_t*)(lm + tl * MP + fl / 8) >> (4 * lhalf);
               uint32_t* loc[4];
               float s[4][2], rt[4][2];
-              bool tiny = false;   // a subnormal s (the raw square root flushes it)
+              // a subnormal s (the raw square root flushes it): a positive
+              // subnormal bf16 is a bit pattern v in [1, 0x7F], i.e. (v - 1)
+              // mod 2^16 < 0x7F; the smallest over the lane's eight values
+              // decides (packed 16-bit integer arithmetic)
+              u16x2 vmin = {0xFFFFu, 0xFFFFu};
 #pragma unroll
               for (int b = 0; b < 4; ++b) {
                 loc[b] = (uint32_t*)(lv + val_word(tl, fl / 4 + 2 * b + lhalf));
                 const uint32_t sv = *loc[b];
                 s[b][0] = __builtin_bit_cast(float, sv << 16);
                 s[b][1] = __builtin_bit_cast(float, sv & 0xFFFF0000u);
-                tiny |= __builtin_amdgcn_classf(s[b][0], 0x80) | __builtin_amdgcn_classf(s[b][1], 0x80);
+                vmin = __builtin_elementwise_min(vmin, __builtin_bit_cast(u16x2, sv) - (u16x2){1u, 1u});
               }
+              const bool tiny = (vmin[0] < vmin[1] ? vmin[0] : vmin[1]) < 0x7Fu;
               if (__builtin_amdgcn_ballot_w64(tiny) == 0) {
 #pragma unroll
                 for (int b = 0; b < 4; ++b)
